@@ -1,0 +1,228 @@
+"""Benchmark of the ProxyAttn prefill hot path on one MI355X.
+
+One step = the whole path on one synthetic layer already resident in HBM:
+proxyattn_estimate -> proxyattn_select_budget -> proxyattn_block_sparse_prefill.
+Default workload: Llama-3-8B-shaped attention layer at 131072 tokens (32 query
+/ 8 KV heads, d 128, block 128, 4 proxy groups, stride 4, gamma 0.95, head
+deviation 0.3), bf16.
+
+Prints ONE JSON line (rank 0).  Besides the step time it reports the stage
+times, the same-build dense kernel's time, dense-equivalent TFLOP/s, the
+estimation overhead, sparsity, a roofline entry for the dominant kernel
+(block-sparse attention, MFMA-bound) and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sparse prefill attention ms + dense-equiv TFLOP/s at 128K; estimation overhead %"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3_8b_n131072")
+    ap.add_argument("--gamma", type=float, default=None)
+    ap.add_argument("--noise", type=float, default=None, help="head deviation sigma")
+    ap.add_argument("--num-proxy-groups", type=int, default=None)
+    ap.add_argument("--min-budget", type=int, default=None)
+    ap.add_argument("--dense-steps", type=int, default=3)
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-rows", type=int, default=8,
+                    help="block rows of the oracle sample (all heads)")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, q, k, v, sample_rows: int):
+    """Time the oracle on a bounded sample and scale it to one full step.
+
+    Sample: the last-block masses and budgets in full (they are per head and
+    small), plus proxy scores, lists and attention for `sample_rows` seeded
+    block rows (all heads).  Per-row costs grow linearly with the row index,
+    so the sampled rows' time is scaled by sum(m+1 over all rows) / sum(m+1
+    over the sample).
+    """
+    from threadpoolctl import threadpool_info
+    from oracle import proxyattn_oracle as O
+    mq = wl.num_blocks
+    rng = np.random.default_rng(12345)
+    rows = np.sort(rng.choice(mq, size=min(sample_rows, mq), replace=False))
+    sc = O.default_scale(wl.head_dim)
+    t0 = time.perf_counter()
+    qg, kg = O.pool_proxy_heads(q, k, wl.num_proxy_groups, wl.stride, wl.dtype)
+    t1 = time.perf_counter()
+    logA, _ = O.proxy_block_logscore(qg, kg, wl.seq_len, wl.block_size, wl.stride, sc, rows=rows)
+    t2 = time.perf_counter()
+    mass = O.lastblock_mass(q, k, wl.block_size, sc)
+    counts, _ = O.budget_counts(mass, wl.gamma, wl.min_budget_tokens, wl.block_size)
+    t3 = time.perf_counter()
+    bc, bi = O.select_blocks(logA, counts, wl.num_q_heads, rows=rows)
+    t4 = time.perf_counter()
+    qrows = np.concatenate([np.arange(m * wl.block_size, min((m + 1) * wl.block_size, wl.seq_len))
+                            for m in rows])
+    O.block_sparse_attention(q, k, v, bc, bi, wl.block_size, sc, query_rows=qrows)
+    t5 = time.perf_counter()
+    weight_all = mq * (mq + 1) / 2
+    weight_s = float(np.sum(rows + 1))
+    scale_rows = weight_all / weight_s
+    full_s = (t1 - t0) + (t3 - t2) + ((t2 - t1) + (t4 - t3) + (t5 - t4)) * scale_rows
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {
+        "value": round(full_s * 1e3, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+        "sample": (f"pooling, last-block masses and budgets in full; proxy scores, lists and "
+                   f"attention for {len(rows)} of {mq} block rows (all heads), scaled by causal "
+                   f"work; measured {t5 - t0:.1f} s"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU: --gpus must be 1 (the path shards "
+                                   "by heads across GPUs only by design)"}))
+        sys.exit(2)
+    import torch
+    from paper_2509_24745_amd import proxyattn as pa
+    from paper_2509_24745_amd.synth import WORKLOADS, generate
+
+    wl = WORKLOADS[args.workload]
+    kw = {}
+    if args.gamma is not None:
+        kw["gamma"] = args.gamma
+    if args.noise is not None:
+        kw["noise"] = args.noise
+    if args.num_proxy_groups is not None:
+        kw["num_proxy_groups"] = args.num_proxy_groups
+    if args.min_budget is not None:
+        kw["min_budget_tokens"] = args.min_budget
+    wl = wl.replace(**kw) if kw else wl
+    print(f"[bench] generating {wl.name} N={wl.seq_len} gamma={wl.gamma} "
+          f"sigma={wl.structure.noise}", file=sys.stderr, flush=True)
+    t = time.time()
+    g = generate(wl)
+    print(f"[bench] generated in {time.time() - t:.1f}s", file=sys.stderr, flush=True)
+    prob = pa.Problem(seq_len=wl.seq_len, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                      head_dim=wl.head_dim, block_size=wl.block_size,
+                      num_proxy_groups=wl.num_proxy_groups, stride=wl.stride, dtype=wl.dtype)
+    dt = prob.torch_dtype
+    q = torch.from_numpy(g["q"]).to(dt).cuda()
+    k = torch.from_numpy(g["k"]).to(dt).cuda()
+    v = torch.from_numpy(g["v"]).to(dt).cuda()
+    bufs = pa.Buffers(prob)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, stream)
+        if ev: ev[1].record(stream)
+        pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma, wl.min_budget_tokens,
+                                   bufs.head_count, bufs.block_count, bufs.block_index, stream)
+        if ev: ev[2].record(stream)
+        pa.proxyattn_block_sparse_prefill(prob, q, k, v, bufs.block_count, bufs.block_index,
+                                          bufs.out, bufs.lse, bufs.workspace, stream)
+        if ev: ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = start.elapsed_time(stop) / args.steps
+    t_est = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    t_sel = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    print(f"[bench] {args.steps} steps: {ms_total:.3f} ms/step (est {t_est:.3f}, sel {t_sel:.3f}, "
+          f"attn {t_attn:.3f}); host wall {wall:.2f}s", file=sys.stderr, flush=True)
+
+    mq, hq, d, b, n = prob.num_blocks, prob.num_q_heads, prob.head_dim, prob.block_size, prob.seq_len
+    total_blocks = int(bufs.block_count.sum().item())
+    causal_blocks = hq * mq * (mq + 1) // 2
+    sparsity = 1.0 - total_blocks / causal_blocks
+    f_dense = 4.0 * hq * d * n * (n + 1) / 2          # dense-equivalent causal flops
+    f_attn = 4.0 * b * b * d * total_blocks            # flops the sparse kernel computes
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    achieved = f_attn / (t_attn * 1e-3) / 1e12
+
+    t_dense = None
+    if not args.no_dense:
+        de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        dense_out = torch.empty_like(bufs.out)
+        pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
+        torch.cuda.synchronize()
+        de[0].record(stream)
+        for _ in range(args.dense_steps):
+            pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
+        de[1].record(stream)
+        torch.cuda.synchronize()
+        t_dense = de[0].elapsed_time(de[1]) / args.dense_steps
+        print(f"[bench] dense {t_dense:.3f} ms", file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, g["q"], g["k"], g["v"], args.cpu_sample_rows)
+
+    line = {
+        "metric": METRIC,
+        "value": round(ms_total, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_total, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "seq_len": n, "num_q_heads": hq,
+                   "num_kv_heads": prob.num_kv_heads, "head_dim": d, "block_size": b,
+                   "num_proxy_groups": prob.num_proxy_groups, "stride": prob.stride,
+                   "gamma": wl.gamma, "head_deviation": wl.structure.noise,
+                   "min_budget_tokens": wl.min_budget_tokens, "parallelism": "single GPU"},
+        "t_estimate_ms": round(t_est, 4),
+        "t_select_ms": round(t_sel, 4),
+        "t_attention_ms": round(t_attn, 4),
+        "dense_equiv_tflops": round(f_dense / (ms_total * 1e-3) / 1e12, 2),
+        "estimation_overhead_pct": round(100.0 * (t_est + t_sel) / ms_total, 2),
+        "sparsity": round(sparsity, 4),
+        "t_dense_ms": round(t_dense, 4) if t_dense else None,
+        "speedup_vs_dense": round(t_dense / ms_total, 3) if t_dense else None,
+        "estimation_overhead_pct_of_dense": round(100.0 * (t_est + t_sel) / t_dense, 2)
+        if t_dense else None,
+        "dense_mfma_frac": round(4.0 * b * b * d * hq * mq * (mq + 1) / 2 / (t_dense * 1e-3)
+                                 / 1e12 / peak, 4) if t_dense else None,
+        "roofline": {"kernel": "attn_kernel (block-sparse prefill call)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,179 @@
+/*
+ * proxyattn.h - C ABI of the ProxyAttn prefill path on MI355X (gfx950).
+ *
+ * ProxyAttn ("Guided Sparse Attention via Representative Heads",
+ * arXiv 2509.24745) speeds up long-context prefill in three steps:
+ *
+ *   1. proxyattn_estimate        proxy-head block scoring (Sec. 3.1, Eq. 1-2)
+ *                                and the per-head last-block attention mass
+ *                                the budget is read from (Alg. 1, first two
+ *                                steps);
+ *   2. proxyattn_select_budget   block-aware dynamic per-head budget (Alg. 1,
+ *                                last two steps) and per-head Top-K block
+ *                                lists (Sec. 3.2, Eq. 3);
+ *   3. proxyattn_block_sparse_prefill
+ *                                causal block-sparse attention over the
+ *                                selected blocks only (Sec. 3.2, last
+ *                                paragraph).
+ *
+ * proxyattn_dense_prefill runs the same attention kernel over every causal
+ * block; it is the dense baseline the sparse path is measured against.
+ *
+ * One sequence, one attention layer, prefill.  Notation: N tokens, Hq query
+ * heads, Hkv key/value heads (GQA: query head i reads KV head i/(Hq/Hkv)),
+ * head dim d, block size b, G proxy groups (contiguous runs of Hq/G query
+ * heads), stride s, Mq = Nk = ceil(N/b) blocks, N' = ceil(N/s) strided tokens.
+ *
+ * Conventions shared by every entry point:
+ *  - Tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned.
+ *    Problem descriptors and scalars are host values.
+ *  - The library never allocates device memory and never synchronises.  Every
+ *    call validates all of its arguments first; a call that returns an error
+ *    has enqueued nothing.  A call that returns PROXYATTN_OK has enqueued its
+ *    kernels, in order, on `stream` (a hipStream_t; NULL = the default stream)
+ *    and returns without waiting.  Faults inside kernels surface at the
+ *    caller's next synchronisation.
+ *  - Calls are stateless and thread-safe.  Calls that share a workspace must
+ *    be ordered (same stream, or synchronised by the caller).
+ *  - Results are bitwise deterministic (no floating-point atomics).
+ *  - N == 0 is a valid empty problem: nothing is enqueued.
+ *  - Inputs must be finite; non-finite inputs give unspecified outputs.
+ */
+#ifndef PROXYATTN_H
+#define PROXYATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define PROXYATTN_OK 0
+#define PROXYATTN_E_INVALID 1     /* null pointer, negative size, gamma out of (0,1], ... */
+#define PROXYATTN_E_UNSUPPORTED 2 /* a shape or dtype this build does not implement */
+#define PROXYATTN_E_WORKSPACE 3   /* workspace smaller than proxyattn_workspace_size */
+#define PROXYATTN_E_HIP 4         /* a kernel launch failed (see proxyattn_last_error) */
+
+/* Element types of Q, K, V and O. */
+#define PROXYATTN_BF16 0
+#define PROXYATTN_F32 1
+
+/*
+ * Problem descriptor.  Q is [N][Hq][d], K and V are [N][Hkv][d], O is
+ * [N][Hq][d]; the innermost dimension d is contiguous.  Token and head
+ * strides are in ELEMENTS; 0 selects the packed default (tok = H*d,
+ * head = d).  Every row start (token*tok_stride + head*head_stride) must be
+ * 16-byte aligned.
+ *
+ * Supported: d in {64, 128}; b in {64, 128}; s in {1, 2, 4} with b/s >= 16;
+ * Hq % Hkv == 0; Hq % G == 0; Nk <= 8192.  bf16 problems compute products on
+ * bf16 MFMA with fp32 accumulation; fp32 problems on fp32 MFMA.
+ */
+typedef struct proxyattn_problem {
+    uint32_t struct_size;      /* = sizeof(proxyattn_problem) */
+    int32_t seq_len;           /* N >= 0 */
+    int32_t num_q_heads;       /* Hq */
+    int32_t num_kv_heads;      /* Hkv */
+    int32_t head_dim;          /* d */
+    int32_t block_size;        /* b */
+    int32_t num_proxy_groups;  /* G */
+    int32_t stride;            /* s: keep tokens t with t % s == 0 (Sec. 3.1) */
+    int32_t dtype;             /* PROXYATTN_BF16 or PROXYATTN_F32 */
+    float softmax_scale;       /* <= 0 selects 1/sqrt(d) */
+    int64_t q_tok_stride, q_head_stride;
+    int64_t kv_tok_stride, kv_head_stride; /* shared by K and V */
+    int64_t o_tok_stride, o_head_stride;
+} proxyattn_problem;
+
+/*
+ * Bytes of device workspace that proxyattn_estimate and the two prefill
+ * entry points need (the largest of their needs; one buffer serves all).
+ * Returns PROXYATTN_OK and writes *bytes, or an error for a bad problem.
+ */
+int proxyattn_workspace_size(const proxyattn_problem* p, size_t* bytes);
+
+/*
+ * Where proxyattn_estimate leaves the pooled proxy heads inside the
+ * workspace: Q^g at workspace+*qg_offset and K^g at workspace+*kg_offset,
+ * each [G][N'][d] in the problem's dtype (packed).  For inspection and tests.
+ */
+int proxyattn_workspace_layout(const proxyattn_problem* p, size_t* qg_offset, size_t* kg_offset);
+
+/*
+ * Step 1: block scoring (Sec. 3.1) and last-block mass (Alg. 1).
+ *
+ *  block_logscore [G][Mq][Nk] fp32 (out): natural log of Eq. 1's
+ *      A^g = maxpool(softmax(Q^g K^g^T / sqrt d)) where Q^g, K^g are the
+ *      group means of Eq. 2 taken on the tokens t % s == 0, rounded to the
+ *      problem dtype; the softmax of strided row t' runs over the strided
+ *      causal keys u' <= t'; the max-pool of block (m, n) runs over its
+ *      strided rows and causal keys.  Entries with n > m are -inf.
+ *  lastblk_mass [Hq][Nk] fp32 (out): per query head i, the attention
+ *      probabilities of the last min(b, N) query tokens over all causal keys,
+ *      computed with the head's own Q and its KV head's K at full
+ *      resolution, summed over those rows and over the keys of each block
+ *      (each row of the output sums to min(b, N)).
+ *  workspace: device buffer of at least proxyattn_workspace_size bytes.
+ */
+int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
+                       float* block_logscore, float* lastblk_mass, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * Step 2: per-head budget (Alg. 1) and block lists (Eq. 3).
+ *
+ *  gamma in (0, 1]: cumulative-probability threshold.  Per head, the masses
+ *      are normalised to sum 1, sorted descending, and the budget is the
+ *      smallest count of leading blocks whose sum reaches gamma (Nk if none;
+ *      Nk for gamma == 1).
+ *  min_budget_tokens >= 0: the count is raised to ceil(min_budget_tokens/b)
+ *      and capped at Nk.
+ *  head_count [Hq] int32 (out): the per-head budget in blocks.
+ *  block_count [Hq][Mq] int32 (out): min(head_count[i], m+1).
+ *  block_index [Hq][Mq][Nk] int32 (out): for head i and block row m, the
+ *      block_count[i][m] causal blocks n <= m with the highest
+ *      block_logscore[g(i)][m][n] (ties to the lower n), in ascending order,
+ *      then -1 up to Nk.
+ */
+int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logscore,
+                            const float* lastblk_mass, float gamma, int32_t min_budget_tokens,
+                            int32_t* head_count, int32_t* block_count, int32_t* block_index,
+                            void* stream);
+
+/*
+ * Step 3: block-sparse causal attention.  For query token t in block m and
+ * head i, out[t][i] = softmax_u(c * <q_t, k_u>) v_u over the keys u <= t of
+ * the blocks block_index[i][m][0 .. block_count[i][m]).  Lists must be
+ * ascending, unique, within 0..m, with 1 <= count <= m+1 (the lists
+ * proxyattn_select_budget writes satisfy this; a row with count 0 gets
+ * out = 0 and lse = -inf).
+ *  out: [N][Hq][d] in the problem's dtype (o strides).
+ *  lse: [Hq][N] fp32 natural-log row log-sum-exp, or NULL.
+ *  workspace: as for proxyattn_estimate (holds a blocked copy of V).
+ */
+int proxyattn_block_sparse_prefill(const proxyattn_problem* p, const void* q, const void* k,
+                                   const void* v, const int32_t* block_count,
+                                   const int32_t* block_index, void* out, float* lse,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Dense causal attention with the same kernels (every block n <= m). */
+int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const void* k,
+                            const void* v, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/* Static text for a return code. */
+const char* proxyattn_error_string(int code);
+
+/* Text of the last error raised on the calling thread ("" if none). */
+const char* proxyattn_last_error(void);
+
+/* Library version, e.g. "0.1.0". */
+const char* proxyattn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PROXYATTN_H */

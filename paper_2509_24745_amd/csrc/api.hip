@@ -1,0 +1,272 @@
+// C ABI of the ProxyAttn prefill path: argument validation, workspace
+// layout and kernel sequencing.  Every entry point validates all of its
+// arguments before enqueuing anything, never allocates and never
+// synchronises.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "proxyattn.h"
+#include "internal.h"
+
+namespace pa {
+
+static thread_local char g_last_error[512] = "";
+
+static int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+static int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+static int hip_fail(hipError_t e, const char* where) {
+    return fail(PROXYATTN_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Validates the descriptor and resolves it into a Shape.
+static int resolve(const proxyattn_problem* p, Shape* sh) {
+    if (!p) return fail(PROXYATTN_E_INVALID, "problem is NULL");
+    if (p->struct_size != sizeof(proxyattn_problem))
+        return fail(PROXYATTN_E_INVALID, "struct_size %u != %zu", p->struct_size,
+                    sizeof(proxyattn_problem));
+    if (p->seq_len < 0) return fail(PROXYATTN_E_INVALID, "seq_len %d < 0", p->seq_len);
+    if (p->num_q_heads <= 0 || p->num_kv_heads <= 0 || p->num_proxy_groups <= 0)
+        return fail(PROXYATTN_E_INVALID, "head and group counts must be positive");
+    if (p->head_dim <= 0 || p->block_size <= 0 || p->stride <= 0)
+        return fail(PROXYATTN_E_INVALID, "head_dim, block_size and stride must be positive");
+    if (p->num_q_heads % p->num_kv_heads)
+        return fail(PROXYATTN_E_UNSUPPORTED, "num_q_heads %% num_kv_heads != 0");
+    if (p->num_q_heads % p->num_proxy_groups)
+        return fail(PROXYATTN_E_UNSUPPORTED, "num_q_heads %% num_proxy_groups != 0");
+    if (p->head_dim != 64 && p->head_dim != 128)
+        return fail(PROXYATTN_E_UNSUPPORTED, "head_dim %d not in {64, 128}", p->head_dim);
+    if (p->block_size != 64 && p->block_size != 128)
+        return fail(PROXYATTN_E_UNSUPPORTED, "block_size %d not in {64, 128}", p->block_size);
+    if (p->stride != 1 && p->stride != 2 && p->stride != 4)
+        return fail(PROXYATTN_E_UNSUPPORTED, "stride %d not in {1, 2, 4}", p->stride);
+    if (p->block_size % p->stride || p->block_size / p->stride < 16)
+        return fail(PROXYATTN_E_UNSUPPORTED, "block_size / stride must be an integer >= 16");
+    if (p->dtype != PROXYATTN_BF16 && p->dtype != PROXYATTN_F32)
+        return fail(PROXYATTN_E_UNSUPPORTED, "dtype %d", p->dtype);
+    if (!(p->softmax_scale == p->softmax_scale) || isinf(p->softmax_scale))
+        return fail(PROXYATTN_E_INVALID, "softmax_scale is not finite");
+    const int64_t mq = ((int64_t)p->seq_len + p->block_size - 1) / p->block_size;
+    if (mq > 8192) return fail(PROXYATTN_E_UNSUPPORTED, "ceil(N/b) = %lld > 8192", (long long)mq);
+    const int esz = p->dtype == PROXYATTN_BF16 ? 2 : 4;
+    const int64_t d = p->head_dim;
+    Shape s{};
+    s.n = p->seq_len;
+    s.hq = p->num_q_heads;
+    s.hkv = p->num_kv_heads;
+    s.d = p->head_dim;
+    s.b = p->block_size;
+    s.g = p->num_proxy_groups;
+    s.s = p->stride;
+    s.dtype = p->dtype;
+    s.mq = (int)mq;
+    s.np = (p->seq_len + p->stride - 1) / p->stride;
+    s.bp = p->block_size / p->stride;
+    s.rep = p->num_q_heads / p->num_kv_heads;
+    s.gsize = p->num_q_heads / p->num_proxy_groups;
+    s.nchunks = (p->seq_len + kMassChunk - 1) / kMassChunk;
+    s.scale = p->softmax_scale > 0.f ? p->softmax_scale : (float)(1.0 / sqrt((double)p->head_dim));
+    s.scale2 = s.scale * 1.4426950408889634f;
+    s.inv_gsize = 1.0f / (float)s.gsize;
+    s.q_tok = p->q_tok_stride ? p->q_tok_stride : (int64_t)p->num_q_heads * d;
+    s.q_head = p->q_head_stride ? p->q_head_stride : d;
+    s.kv_tok = p->kv_tok_stride ? p->kv_tok_stride : (int64_t)p->num_kv_heads * d;
+    s.kv_head = p->kv_head_stride ? p->kv_head_stride : d;
+    s.o_tok = p->o_tok_stride ? p->o_tok_stride : (int64_t)p->num_q_heads * d;
+    s.o_head = p->o_head_stride ? p->o_head_stride : d;
+    const int64_t strides[6] = {s.q_tok, s.q_head, s.kv_tok, s.kv_head, s.o_tok, s.o_head};
+    for (int j = 0; j < 6; ++j) {
+        if (strides[j] < 0) return fail(PROXYATTN_E_INVALID, "negative stride");
+        if ((strides[j] * esz) % 16)
+            return fail(PROXYATTN_E_UNSUPPORTED, "strides must keep rows 16-byte aligned");
+    }
+    *sh = s;
+    return PROXYATTN_OK;
+}
+
+WsLayout ws_layout(const Shape& sh) {
+    const size_t esz = sh.dtype == PROXYATTN_BF16 ? 2 : 4;
+    WsLayout L{};
+    size_t off = 0;
+    L.qg = off;   off = align_up(off + (size_t)sh.g * sh.np * sh.d * esz);
+    L.kg = off;   off = align_up(off + (size_t)sh.g * sh.np * sh.d * esz);
+    L.lse2 = off; off = align_up(off + (size_t)sh.g * sh.np * 4);
+    L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
+    L.part = off; off = align_up(off + (size_t)sh.hq * sh.nchunks * sh.b * 2 * 4);
+    L.vt = off;   off = align_up(off + (size_t)sh.hkv * sh.mq * sh.d * sh.b * esz);
+    L.total = off;
+    return L;
+}
+
+static int check_ws(const Shape& sh, const void* ws, size_t bytes, WsLayout* L) {
+    *L = ws_layout(sh);
+    if (!ws) return fail(PROXYATTN_E_INVALID, "workspace is NULL");
+    if (!aligned16(ws)) return fail(PROXYATTN_E_INVALID, "workspace not 16-byte aligned");
+    if (bytes < L->total)
+        return fail(PROXYATTN_E_WORKSPACE, "workspace %zu bytes < %zu needed", bytes, L->total);
+    return PROXYATTN_OK;
+}
+
+static int check_ptr(const void* p, const char* name) {
+    if (!p) return fail(PROXYATTN_E_INVALID, "%s is NULL", name);
+    if (!aligned16(p)) return fail(PROXYATTN_E_INVALID, "%s not 16-byte aligned", name);
+    return PROXYATTN_OK;
+}
+
+#define PA_TRY(expr)                         \
+    do {                                     \
+        const int rc_ = (expr);              \
+        if (rc_ != PROXYATTN_OK) return rc_; \
+    } while (0)
+
+#define PA_LAUNCH(expr, where)                        \
+    do {                                              \
+        const hipError_t e_ = (expr);                 \
+        if (e_ != hipSuccess) return hip_fail(e_, where); \
+    } while (0)
+
+}  // namespace pa
+
+using namespace pa;
+
+extern "C" {
+
+int proxyattn_workspace_size(const proxyattn_problem* p, size_t* bytes) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (!bytes) return fail(PROXYATTN_E_INVALID, "bytes is NULL");
+    *bytes = sh.n == 0 ? 0 : ws_layout(sh).total;
+    return PROXYATTN_OK;
+}
+
+int proxyattn_workspace_layout(const proxyattn_problem* p, size_t* qg_offset, size_t* kg_offset) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (!qg_offset || !kg_offset) return fail(PROXYATTN_E_INVALID, "offset pointer is NULL");
+    const WsLayout L = ws_layout(sh);
+    *qg_offset = L.qg;
+    *kg_offset = L.kg;
+    return PROXYATTN_OK;
+}
+
+int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
+                       float* block_logscore, float* lastblk_mass, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(q, "q"));
+    PA_TRY(check_ptr(k, "k"));
+    PA_TRY(check_ptr(block_logscore, "block_logscore"));
+    PA_TRY(check_ptr(lastblk_mass, "lastblk_mass"));
+    WsLayout L;
+    PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    PA_LAUNCH(launch_pool(sh, q, k, ws + L.qg, ws + L.kg, st), "pool");
+    PA_LAUNCH(launch_est_rowmax(sh, ws + L.qg, ws + L.kg, (float*)(ws + L.rbm),
+                                (float*)(ws + L.lse2), st), "est_rowmax");
+    PA_LAUNCH(launch_est_reduce(sh, (const float*)(ws + L.rbm), (const float*)(ws + L.lse2),
+                                block_logscore, st), "est_reduce");
+    PA_LAUNCH(launch_mass(sh, q, k, (float*)(ws + L.part), lastblk_mass, st), "mass");
+    return PROXYATTN_OK;
+}
+
+int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logscore,
+                            const float* lastblk_mass, float gamma, int32_t min_budget_tokens,
+                            int32_t* head_count, int32_t* block_count, int32_t* block_index,
+                            void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (!(gamma > 0.f && gamma <= 1.f))
+        return fail(PROXYATTN_E_INVALID, "gamma must lie in (0, 1]");
+    if (min_budget_tokens < 0) return fail(PROXYATTN_E_INVALID, "min_budget_tokens < 0");
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(block_logscore, "block_logscore"));
+    PA_TRY(check_ptr(lastblk_mass, "lastblk_mass"));
+    PA_TRY(check_ptr(head_count, "head_count"));
+    PA_TRY(check_ptr(block_count, "block_count"));
+    PA_TRY(check_ptr(block_index, "block_index"));
+    const int64_t min_blocks64 = ((int64_t)min_budget_tokens + sh.b - 1) / sh.b;
+    const int min_blocks = (int)(min_blocks64 > sh.mq ? sh.mq : min_blocks64);
+    hipStream_t st = (hipStream_t)stream;
+    PA_LAUNCH(launch_budget(sh, lastblk_mass, gamma, min_blocks, head_count, st), "budget");
+    PA_LAUNCH(launch_select(sh, block_logscore, head_count, block_count, block_index, st),
+              "select");
+    return PROXYATTN_OK;
+}
+
+static int prefill_common(const proxyattn_problem* p, const void* q, const void* k,
+                          const void* v, const int32_t* block_count, const int32_t* block_index,
+                          void* out, float* lse, void* workspace, size_t workspace_bytes,
+                          void* stream, bool dense) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(q, "q"));
+    PA_TRY(check_ptr(k, "k"));
+    PA_TRY(check_ptr(v, "v"));
+    PA_TRY(check_ptr(out, "out"));
+    if (!dense) {
+        PA_TRY(check_ptr(block_count, "block_count"));
+        PA_TRY(check_ptr(block_index, "block_index"));
+    }
+    if (lse && ((uintptr_t)lse & 3u)) return fail(PROXYATTN_E_INVALID, "lse not 4-byte aligned");
+    WsLayout L;
+    PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    PA_LAUNCH(launch_vt(sh, v, ws + L.vt, st), "v_blocked");
+    PA_LAUNCH(launch_attention(sh, dense, q, k, ws + L.vt, block_count, block_index, out, lse, st),
+              "attention");
+    return PROXYATTN_OK;
+}
+
+int proxyattn_block_sparse_prefill(const proxyattn_problem* p, const void* q, const void* k,
+                                   const void* v, const int32_t* block_count,
+                                   const int32_t* block_index, void* out, float* lse,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+    return prefill_common(p, q, k, v, block_count, block_index, out, lse, workspace,
+                          workspace_bytes, stream, false);
+}
+
+int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const void* k,
+                            const void* v, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+    return prefill_common(p, q, k, v, nullptr, nullptr, out, lse, workspace, workspace_bytes,
+                          stream, true);
+}
+
+const char* proxyattn_error_string(int code) {
+    switch (code) {
+        case PROXYATTN_OK: return "ok";
+        case PROXYATTN_E_INVALID: return "invalid argument";
+        case PROXYATTN_E_UNSUPPORTED: return "unsupported problem";
+        case PROXYATTN_E_WORKSPACE: return "workspace too small";
+        case PROXYATTN_E_HIP: return "HIP launch failure";
+        default: return "unknown error";
+    }
+}
+
+const char* proxyattn_last_error(void) { return g_last_error; }
+
+const char* proxyattn_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,414 @@
+// Block scoring (Sec. 3.1, Eq. 1) and the last-block attention mass the
+// per-head budget is read from (Alg. 1, first two steps).
+//
+// All score tiles are computed transposed, S^T = K Q^T, on the 32x32 MFMA
+// tile: lane l then owns one query (column l % 32) and 16 keys of it, so row
+// statistics (max, sum) are lane-local plus one exchange between the two
+// wave halves.  Key tiles of 32 rows are staged through LDS (double
+// buffered) and shared by the 4 waves of a workgroup; query fragments stay in
+// registers for the whole key loop.
+//
+// Proxy scores (a2 + a3):
+//   est_rowmax: one pass over the strided causal keys per strided query row,
+//     giving the row log2-sum-exp L2[t'] and, for every key block n <= m, the
+//     row's largest scaled logit in that block, rbm[m, n][t' - m b'].
+//   est_reduce: logA[m, n] = ln2 * max_{t' in m} (rbm[m, n][t'] - L2[t'])
+//     = log max_{t', u'} softmax(...)  (the max-pool of Eq. 1, log domain).
+// One MFMA pass instead of two (no recomputation of the tiles to re-derive
+// the max-pool after the row normaliser is known); rbm costs
+// G * Mq(Mq+1)/2 * b' * 4 bytes of workspace.
+//
+// Last-block mass (a4): the last min(b, N) query tokens of every head
+// against all keys, split into key chunks for parallelism.
+//   mass_partial: per (head, chunk) the rows' partial (max, sum).
+//   mass_final:   combines the partials into each row's normaliser, recomputes
+//     the tiles and sums exp(S - L) per key block over keys and rows.
+#include "common.h"
+#include "internal.h"
+
+namespace pa {
+
+// Stages a tile of 32 consecutive key rows [row0, row0 + 32) x D (row-major,
+// `ld` elements between rows, rows >= nrows read as zero) through registers
+// into an LDS tile with rows padded by 16 bytes.
+template <typename T, int D, int NTH>
+struct KeyTile {
+    static constexpr int V = Vec16<T>::n;
+    static constexpr int LDT = D + V;
+    static constexpr int VECS = 32 * D / V;
+    static constexpr int PER = (VECS + NTH - 1) / NTH;
+    u32x4 reg[PER];
+
+    __device__ __forceinline__ void load(const T* base, int64_t ld, int row0, int nrows, int tid) {
+#pragma unroll
+        for (int c = 0; c < PER; ++c) {
+            const int vi = tid + c * NTH;
+            if (PER * NTH == VECS || vi < VECS) {
+                const int row = vi / (D / V), col = (vi % (D / V)) * V;
+                if (row0 + row < nrows)
+                    reg[c] = *reinterpret_cast<const u32x4*>(base + (int64_t)(row0 + row) * ld + col);
+                else
+                    reg[c] = zero_u32x4();
+            }
+        }
+    }
+    __device__ __forceinline__ void store(T* lds, int tid) const {
+#pragma unroll
+        for (int c = 0; c < PER; ++c) {
+            const int vi = tid + c * NTH;
+            if (PER * NTH == VECS || vi < VECS) {
+                const int row = vi / (D / V), col = (vi % (D / V)) * V;
+                *reinterpret_cast<u32x4*>(lds + row * LDT + col) = reg[c];
+            }
+        }
+    }
+};
+
+// S^T tile (32 keys x 32 queries) of one wave: keys from an LDS tile,
+// queries from register fragments.  Lane (lc, h) receives the 16 keys
+// c_row(r, h) of query lc.
+template <typename T, int D>
+__device__ __forceinline__ f32x16 st_tile(const T* lds_tile, const typename FragOf<T>::type* qf,
+                                          int lc, int h) {
+    constexpr int LDT = D + Vec16<T>::n;
+    f32x16 acc = zero16();
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+        mma(acc, load_frag<T>(lds_tile + lc * LDT + 16 * ks + 8 * h), qf[ks]);
+    return acc;
+}
+
+// ---------------------------------------------------------------------------
+// a2: proxy row normaliser and per-(row, key block) max
+// grid (ceil(N'/128), G), 256 threads; wave w owns strided rows R0+32w..+31.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int BP>
+__global__ __launch_bounds__(256) void est_rowmax_kernel(Shape sh, const T* __restrict__ qg,
+                                                         const T* __restrict__ kg,
+                                                         float* __restrict__ rbm,
+                                                         float* __restrict__ lse2) {
+    typedef typename FragOf<T>::type Frag;
+    constexpr int KS = D / 16;
+    __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, 256>::LDT];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
+    const int g = blockIdx.y;
+    const int np = sh.np;
+    const int R0 = blockIdx.x * 128;
+    const T* qbase = qg + (int64_t)g * np * D;
+    const T* kbase = kg + (int64_t)g * np * D;
+    const int row = R0 + 32 * w + lc;
+    const bool wave_on = R0 + 32 * w < np;
+    const int wave_last_tile = wave_on ? min(R0 + 32 * w + 31, np - 1) / 32 : -1;
+    const int last_tile = min(R0 + 127, np - 1) / 32;
+
+    Frag qf[KS];
+    {
+        const T* qrow = qbase + (int64_t)min(row, np - 1) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
+    }
+    const int64_t tri_total = (int64_t)sh.mq * (sh.mq + 1) / 2;
+    float* rbm_g = rbm + (int64_t)g * tri_total * BP;
+
+    float m = kNegInf, l = 0.f, bm = kNegInf;
+    KeyTile<T, D, 256> kt_ld;
+    kt_ld.load(kbase, D, 0, np, tid);
+    kt_ld.store(tiles[0], tid);
+    __syncthreads();
+    for (int kt = 0; kt <= last_tile; ++kt) {
+        if (kt < last_tile) kt_ld.load(kbase, D, (kt + 1) * 32, np, tid);
+        if (kt <= wave_last_tile) {
+            const f32x16 acc = st_tile<T, D>(tiles[kt & 1], qf, lc, h);
+            float x[16];
+            float tm = kNegInf;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int u = kt * 32 + c_row(r, h);
+                x[r] = (u <= row) ? acc[r] * sh.scale2 : kNegInf;
+                tm = fmaxf(tm, x[r]);
+            }
+            const float mn = fmaxf(m, tm);
+            if (mn != kNegInf) {
+                float sum = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) sum += exp2f(x[r] - mn);
+                l = l * exp2f(m - mn) + sum;
+                m = mn;
+            }
+            if constexpr (BP == 16) {
+                // one 32-key tile holds two key blocks: slots r < 8 and r >= 8
+                float s0 = kNegInf, s1 = kNegInf;
+#pragma unroll
+                for (int r = 0; r < 8; ++r) { s0 = fmaxf(s0, x[r]); s1 = fmaxf(s1, x[r + 8]); }
+                s0 = fmaxf(s0, swap_halves(s0));
+                s1 = fmaxf(s1, swap_halves(s1));
+                if (h == 0 && row < np) {
+                    const int mr = row / 16, j = row % 16, n0 = 2 * kt;
+                    if (n0 <= mr) rbm_g[tri_index(mr, n0) * 16 + j] = s0;
+                    if (n0 + 1 <= mr) rbm_g[tri_index(mr, n0 + 1) * 16 + j] = s1;
+                }
+            } else {
+                constexpr int TPB = BP / 32;  // key tiles per block
+                const float sm = fmaxf(tm, swap_halves(tm));
+                bm = (kt % TPB == 0) ? sm : fmaxf(bm, sm);
+                if ((kt % TPB == TPB - 1 || kt == wave_last_tile) && h == 0 && row < np) {
+                    const int mr = row / BP, j = row % BP, n = kt / TPB;
+                    rbm_g[tri_index(mr, n) * BP + j] = bm;
+                }
+            }
+        }
+        if (kt < last_tile) kt_ld.store(tiles[(kt + 1) & 1], tid);
+        __syncthreads();
+    }
+    const float mo = swap_halves(m), lo = swap_halves(l);
+    const float mm = fmaxf(m, mo);
+    if (h == 0 && row < np) {
+        const float ll = l * exp2f(m - mm) + lo * exp2f(mo - mm);
+        lse2[(int64_t)g * np + row] = mm + log2f(ll);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// a3: block max-pool in the log domain.  grid (Mq, G), 256 threads.
+// ---------------------------------------------------------------------------
+template <int BP>
+__global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* __restrict__ rbm,
+                                                         const float* __restrict__ lse2,
+                                                         float* __restrict__ logA) {
+    __shared__ float L[BP];
+    const int m = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+    const int r0 = m * BP;
+    const int nr = min(BP, sh.np - r0);
+    for (int j = tid; j < BP; j += 256) L[j] = j < nr ? lse2[(int64_t)g * sh.np + r0 + j] : 0.f;
+    __syncthreads();
+    const int64_t tri_total = (int64_t)sh.mq * (sh.mq + 1) / 2;
+    const float* base = rbm + ((int64_t)g * tri_total + tri_index(m, 0)) * BP;
+    float* out = logA + ((int64_t)g * sh.mq + m) * sh.mq;
+    for (int n = tid; n < sh.mq; n += 256) {
+        float v = kNegInf;
+        if (n <= m) {
+            const float* p = base + (int64_t)n * BP;
+            if (nr == BP) {
+#pragma unroll
+                for (int j = 0; j < BP; j += 4) {
+                    const f32x4 x = *reinterpret_cast<const f32x4*>(p + j);
+                    v = fmaxf(v, fmaxf(fmaxf(x[0] - L[j], x[1] - L[j + 1]),
+                                       fmaxf(x[2] - L[j + 2], x[3] - L[j + 3])));
+                }
+            } else {
+                for (int j = 0; j < nr; ++j) v = fmaxf(v, p[j] - L[j]);
+            }
+            v *= kLn2;
+        }
+        out[n] = v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// a4: last-block mass.  grid (nchunks, Hq), B*2 threads (B/32 waves).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int B>
+__global__ __launch_bounds__(B * 2) void mass_partial_kernel(Shape sh, const T* __restrict__ q,
+                                                             const T* __restrict__ k,
+                                                             float* __restrict__ part) {
+    typedef typename FragOf<T>::type Frag;
+    constexpr int NTH = B * 2;
+    __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, NTH>::LDT];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
+    const int c = blockIdx.x, i = blockIdx.y, kvh = i / sh.rep;
+    const int n = sh.n;
+    const int nrows = min(B, n), t0 = n - nrows;
+    const int rl = 32 * w + lc, t = t0 + rl;
+    const bool wave_on = 32 * w < nrows;
+    const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
+    const int key0 = c * kMassChunk, key1 = min(key0 + kMassChunk, n);
+    const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
+    const T* kbase = k + (int64_t)kvh * sh.kv_head;
+
+    Frag qf[D / 16];
+    {
+        const T* qrow = q + (int64_t)min(t, n - 1) * sh.q_tok + (int64_t)i * sh.q_head;
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
+    }
+    float m = kNegInf, l = 0.f;
+    KeyTile<T, D, NTH> ld;
+    ld.load(kbase, sh.kv_tok, kt0 * 32, n, tid);
+    ld.store(tiles[0], tid);
+    __syncthreads();
+    for (int kt = kt0; kt <= kt1; ++kt) {
+        const int buf = (kt - kt0) & 1;
+        if (kt < kt1) ld.load(kbase, sh.kv_tok, (kt + 1) * 32, n, tid);
+        if (wave_on && kt * 32 <= wave_last_t) {
+            const f32x16 acc = st_tile<T, D>(tiles[buf], qf, lc, h);
+            float x[16];
+            float tm = kNegInf;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int u = kt * 32 + c_row(r, h);
+                x[r] = (u <= t) ? acc[r] * sh.scale2 : kNegInf;
+                tm = fmaxf(tm, x[r]);
+            }
+            const float mn = fmaxf(m, tm);
+            if (mn != kNegInf) {
+                float sum = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) sum += exp2f(x[r] - mn);
+                l = l * exp2f(m - mn) + sum;
+                m = mn;
+            }
+        }
+        if (kt < kt1) ld.store(tiles[buf ^ 1], tid);
+        __syncthreads();
+    }
+    const float mo = swap_halves(m), lo = swap_halves(l);
+    const float mm = fmaxf(m, mo);
+    if (h == 0 && rl < nrows) {
+        const float ll = (mm == kNegInf) ? 0.f : l * exp2f(m - mm) + lo * exp2f(mo - mm);
+        float* pp = part + (((int64_t)i * sh.nchunks + c) * B + rl) * 2;
+        pp[0] = mm;
+        pp[1] = ll;
+    }
+}
+
+template <typename T, int D, int B>
+__global__ __launch_bounds__(B * 2) void mass_final_kernel(Shape sh, const T* __restrict__ q,
+                                                           const T* __restrict__ k,
+                                                           const float* __restrict__ part,
+                                                           float* __restrict__ mass) {
+    typedef typename FragOf<T>::type Frag;
+    constexpr int NTH = B * 2, NW = B / 32;
+    constexpr int BPC = kMassChunk / B;  // blocks per chunk
+    __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, NTH>::LDT];
+    __shared__ float wpart[NW][BPC];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
+    const int c = blockIdx.x, i = blockIdx.y, kvh = i / sh.rep;
+    const int n = sh.n;
+    const int nrows = min(B, n), t0 = n - nrows;
+    const int rl = 32 * w + lc, t = t0 + rl;
+    const bool wave_on = 32 * w < nrows;
+    const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
+    const int key0 = c * kMassChunk, key1 = min(key0 + kMassChunk, n);
+    const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
+    const int blk0 = key0 / B, nblk = (key1 - key0 + B - 1) / B;
+    const T* kbase = k + (int64_t)kvh * sh.kv_head;
+
+    // the row's normaliser from all chunks' partials, in chunk order
+    float L2 = 0.f;
+    if (rl < nrows) {
+        const float* pp = part + ((int64_t)i * sh.nchunks * B + rl) * 2;
+        float mx = kNegInf;
+        for (int cc = 0; cc < sh.nchunks; ++cc) mx = fmaxf(mx, pp[(int64_t)cc * B * 2]);
+        float s = 0.f;
+        for (int cc = 0; cc < sh.nchunks; ++cc) {
+            const float mc = pp[(int64_t)cc * B * 2], lcc = pp[(int64_t)cc * B * 2 + 1];
+            if (mc != kNegInf) s += lcc * exp2f(mc - mx);
+        }
+        L2 = mx + log2f(s);
+    }
+    Frag qf[D / 16];
+    {
+        const T* qrow = q + (int64_t)min(t, n - 1) * sh.q_tok + (int64_t)i * sh.q_head;
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
+    }
+    KeyTile<T, D, NTH> ld;
+    ld.load(kbase, sh.kv_tok, kt0 * 32, n, tid);
+    ld.store(tiles[0], tid);
+    __syncthreads();
+    float acc_blk = 0.f;
+    for (int kt = kt0; kt <= kt1; ++kt) {
+        const int buf = (kt - kt0) & 1;
+        if (kt < kt1) ld.load(kbase, sh.kv_tok, (kt + 1) * 32, n, tid);
+        if (wave_on && kt * 32 <= wave_last_t) {
+            const f32x16 acc = st_tile<T, D>(tiles[buf], qf, lc, h);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int u = kt * 32 + c_row(r, h);
+                const float p = (u <= t && rl < nrows) ? exp2f(acc[r] * sh.scale2 - L2) : 0.f;
+                acc_blk += p;
+            }
+        }
+        if (((kt + 1) * 32) % B == 0 || kt == kt1) {
+            const float s = wave_sum(acc_blk);
+            if (lane == 0) wpart[w][(kt * 32) / B - blk0] = s;
+            acc_blk = 0.f;
+        }
+        if (kt < kt1) ld.store(tiles[buf ^ 1], tid);
+        __syncthreads();
+    }
+    for (int bl = tid; bl < nblk; bl += NTH) {
+        float s = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) s += wpart[ww][bl];
+        mass[(int64_t)i * sh.mq + blk0 + bl] = s;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+static hipError_t rowmax_t(const Shape& sh, const void* qg, const void* kg, float* rbm,
+                           float* lse2, hipStream_t st) {
+    dim3 grid((sh.np + 127) / 128, sh.g);
+    switch (sh.bp) {
+        case 16: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 16>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
+        case 32: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 32>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
+        case 64: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 64>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
+        case 128: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 128>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
+                             float* lse2, hipStream_t st) {
+    if (sh.dtype == 0)
+        return sh.d == 64 ? rowmax_t<bf16, 64>(sh, qg, kg, rbm, lse2, st)
+                          : rowmax_t<bf16, 128>(sh, qg, kg, rbm, lse2, st);
+    return sh.d == 64 ? rowmax_t<float, 64>(sh, qg, kg, rbm, lse2, st)
+                      : rowmax_t<float, 128>(sh, qg, kg, rbm, lse2, st);
+}
+
+hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float* lse2, float* logA,
+                             hipStream_t st) {
+    dim3 grid(sh.mq, sh.g);
+    switch (sh.bp) {
+        case 16: hipLaunchKernelGGL((est_reduce_kernel<16>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
+        case 32: hipLaunchKernelGGL((est_reduce_kernel<32>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
+        case 64: hipLaunchKernelGGL((est_reduce_kernel<64>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
+        case 128: hipLaunchKernelGGL((est_reduce_kernel<128>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <typename T, int D, int B>
+static hipError_t mass_t(const Shape& sh, const void* q, const void* k, float* part, float* mass,
+                         hipStream_t st) {
+    dim3 grid(sh.nchunks, sh.hq);
+    hipLaunchKernelGGL((mass_partial_kernel<T, D, B>), grid, dim3(B * 2), 0, st, sh, (const T*)q,
+                       (const T*)k, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((mass_final_kernel<T, D, B>), grid, dim3(B * 2), 0, st, sh, (const T*)q,
+                       (const T*)k, (const float*)part, mass);
+    return hipGetLastError();
+}
+
+hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float* part, float* mass,
+                       hipStream_t st) {
+    if (sh.dtype == 0) {
+        if (sh.d == 64) return sh.b == 64 ? mass_t<bf16, 64, 64>(sh, q, k, part, mass, st)
+                                          : mass_t<bf16, 64, 128>(sh, q, k, part, mass, st);
+        return sh.b == 64 ? mass_t<bf16, 128, 64>(sh, q, k, part, mass, st)
+                          : mass_t<bf16, 128, 128>(sh, q, k, part, mass, st);
+    }
+    if (sh.d == 64) return sh.b == 64 ? mass_t<float, 64, 64>(sh, q, k, part, mass, st)
+                                      : mass_t<float, 64, 128>(sh, q, k, part, mass, st);
+    return sh.b == 64 ? mass_t<float, 128, 64>(sh, q, k, part, mass, st)
+                      : mass_t<float, 128, 128>(sh, q, k, part, mass, st);
+}
+
+}  // namespace pa

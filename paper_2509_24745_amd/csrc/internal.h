@@ -1,0 +1,66 @@
+// Host-side declarations shared by the C-ABI entry points and the kernel
+// launchers.  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pa {
+
+// A validated problem with every derived size resolved.  Passed to kernels
+// by value.
+struct Shape {
+    int n;        // N tokens
+    int hq, hkv;  // query / KV heads
+    int d;        // head dim
+    int b;        // block size
+    int g;        // proxy groups
+    int s;        // stride
+    int dtype;    // PROXYATTN_BF16 / PROXYATTN_F32
+    int mq;       // ceil(N / b) = Nk
+    int np;       // ceil(N / s) strided tokens
+    int bp;       // b / s strided tokens per block
+    int rep;      // Hq / Hkv
+    int gsize;    // Hq / G
+    int nchunks;  // key chunks of the last-block mass kernels
+    float scale;  // softmax scale c
+    float scale2; // c * log2(e)
+    float inv_gsize;  // fl32(1 / |G|)
+    int64_t q_tok, q_head, kv_tok, kv_head, o_tok, o_head;  // element strides
+};
+
+// Keys per chunk of the last-block mass kernels (a multiple of every block size).
+constexpr int kMassChunk = 2048;
+
+// Byte offsets of the workspace regions (each 256-byte aligned).
+struct WsLayout {
+    size_t qg, kg;   // pooled proxy heads [G][N'][d] (problem dtype)
+    size_t lse2;     // proxy row log2-sum-exp [G][N'] fp32
+    size_t rbm;      // per-(row, key block) max of the scaled proxy logits,
+                     // [G][Mq(Mq+1)/2][b'] fp32 (lower-triangular block pairs)
+    size_t part;     // last-block partial (max, sum) [Hq][nchunks][b][2] fp32
+    size_t vt;       // blocked, transposed V [Hkv][Mq][d][b] (problem dtype)
+    size_t total;
+};
+
+WsLayout ws_layout(const Shape& sh);
+
+hipError_t launch_pool(const Shape& sh, const void* q, const void* k, void* qg, void* kg,
+                       hipStream_t st);
+hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
+                             float* lse2, hipStream_t st);
+hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float* lse2, float* logA,
+                             hipStream_t st);
+hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float* part, float* mass,
+                       hipStream_t st);
+hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,
+                         int* head_count, hipStream_t st);
+hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
+                         int* block_count, int* block_index, hipStream_t st);
+hipError_t launch_vt(const Shape& sh, const void* v, void* vt, hipStream_t st);
+hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* k,
+                            const void* vt, const int* block_count, const int* block_index,
+                            void* out, float* lse, hipStream_t st);
+
+}  // namespace pa

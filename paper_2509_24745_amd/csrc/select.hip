@@ -1,0 +1,189 @@
+// Block-aware budget (Alg. 1, last two steps) and per-head Top-K block
+// lists (Sec. 3.2, Eq. 3).
+//
+// budget: one workgroup per query head.  The head's last-block masses are
+//   normalised to sum 1 (Alg. 1 normalises the pooled block scores), sorted
+//   descending in LDS (bitonic), prefix-summed with a wavefront scan, and
+//   the first prefix reaching gamma gives the count k*+1 (Nk if none, Nk for
+//   gamma >= 1), then raised to the minimum budget and capped at Nk.
+// select: one workgroup per (proxy group, block row m).  The m+1 causal
+//   candidates are sorted by (score descending, index ascending) as 64-bit
+//   keys in LDS; every head of the group keeps the candidates whose rank is
+//   below min(count_i, m+1), compacted in ascending block order with
+//   wavefront ballots, and pads its row with -1.
+#include "common.h"
+#include "internal.h"
+
+namespace pa {
+
+// In-place bitonic sort of a[0..P) (P a power of two), ascending.
+template <typename K>
+__device__ void bitonic_sort_asc(K* a, int P, int tid, int nth) {
+    for (int size = 2; size <= P; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int t = tid; t < P / 2; t += nth) {
+                const int i = 2 * t - (t & (stride - 1));
+                const int j = i + stride;
+                const bool up = (i & size) == 0;
+                const K x = a[i], y = a[j];
+                if (up ? (x > y) : (x < y)) { a[i] = y; a[j] = x; }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+static __host__ __device__ inline int next_pow2(int x) {
+    int p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// ---------------------------------------------------------------------------
+// budget: grid Hq, 1024 threads
+// ---------------------------------------------------------------------------
+constexpr int kBudgetThreads = 1024;
+constexpr int kMaxBlocks = 8192;
+
+__global__ __launch_bounds__(kBudgetThreads) void budget_kernel(Shape sh,
+                                                                const float* __restrict__ mass,
+                                                                float gamma, int min_blocks,
+                                                                int* __restrict__ head_count) {
+    __shared__ float a[kMaxBlocks];
+    __shared__ float wtot[kBudgetThreads / 64];
+    __shared__ int hit;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int i = blockIdx.x, nk = sh.mq;
+    const int P = next_pow2(nk);
+    const float* mrow = mass + (int64_t)i * nk;
+
+    // total mass (fixed-order reduction)
+    float part = 0.f;
+    for (int n = tid; n < nk; n += kBudgetThreads) part += mrow[n];
+    part = wave_sum(part);
+    if (lane == 0) wtot[w] = part;
+    if (tid == 0) hit = nk;
+    __syncthreads();
+    float total = 0.f;
+    for (int j = 0; j < kBudgetThreads / 64; ++j) total += wtot[j];
+    // normalised block shares, padded with -1 (sorted to the end)
+    for (int n = tid; n < P; n += kBudgetThreads) a[n] = n < nk ? mrow[n] / total : -1.f;
+    __syncthreads();
+    // descending order = ascending order of the negated values
+    for (int n = tid; n < P; n += kBudgetThreads) a[n] = -a[n];
+    __syncthreads();
+    bitonic_sort_asc<float>(a, P, tid, kBudgetThreads);
+    // inclusive prefix sums: each thread owns E consecutive entries
+    const int E = (P + kBudgetThreads - 1) / kBudgetThreads;
+    const int e0 = tid * E;
+    float own = 0.f;
+    for (int e = 0; e < E; ++e) {
+        const int n = e0 + e;
+        if (n < nk) own += -a[n];
+    }
+    float incl = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const float y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    float excl_w = __shfl_up(incl, 1);
+    if (lane == 0) excl_w = 0.f;
+    __syncthreads();
+    if (lane == 63) wtot[w] = incl;
+    __syncthreads();
+    float base = 0.f;
+    for (int j = 0; j < w; ++j) base += wtot[j];
+    float run = base + excl_w;
+    if (gamma < 1.f) {
+        for (int e = 0; e < E; ++e) {
+            const int n = e0 + e;
+            if (n >= nk) break;
+            run += -a[n];
+            if (run >= gamma) { atomicMin(&hit, n); break; }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int c = (gamma < 1.f && hit < nk) ? hit + 1 : nk;
+        c = max(c, min_blocks);
+        c = min(c, nk);
+        head_count[i] = c;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// select: grid (Mq, G), 256 threads, dynamic LDS = P * 12 bytes
+// ---------------------------------------------------------------------------
+constexpr int kSelectThreads = 256;
+
+__global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
+                                                                const float* __restrict__ logA,
+                                                                const int* __restrict__ head_count,
+                                                                int* __restrict__ block_count,
+                                                                int* __restrict__ block_index) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+    __shared__ int wcount[kSelectThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int m = blockIdx.x, g = blockIdx.y, nk = sh.mq;
+    const int ncand = m + 1;
+    const int P = next_pow2(ncand);
+    const int Pmax = next_pow2(nk);
+    uint64_t* key = reinterpret_cast<uint64_t*>(smem_raw);
+    int* rank = reinterpret_cast<int*>(smem_raw + (size_t)Pmax * 8);
+    const float* srow = logA + ((int64_t)g * sh.mq + m) * nk;
+    // key: (order of -score) << 32 | index  -> ascending = score desc, index asc
+    for (int n = tid; n < P; n += kSelectThreads) {
+        uint64_t kk = ~0ull;
+        if (n < ncand) kk = ((uint64_t)(~float_order_key(srow[n])) << 32) | (uint32_t)n;
+        key[n] = kk;
+    }
+    __syncthreads();
+    bitonic_sort_asc<uint64_t>(key, P, tid, kSelectThreads);
+    for (int p = tid; p < ncand; p += kSelectThreads) rank[(int)(key[p] & 0xffffffffu)] = p;
+    __syncthreads();
+    for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
+        const int kk = min(head_count[i], ncand);
+        int* out = block_index + ((int64_t)i * sh.mq + m) * nk;
+        int base = 0;
+        for (int c0 = 0; c0 < ncand; c0 += kSelectThreads) {
+            const int n = c0 + tid;
+            const bool sel = n < ncand && rank[n] < kk;
+            const uint64_t bal = __ballot(sel);
+            const int before = __popcll(bal & ((1ull << lane) - 1ull));
+            if (lane == 0) wcount[w] = __popcll(bal);
+            __syncthreads();
+            int off = base;
+            for (int j = 0; j < w; ++j) off += wcount[j];
+            int tot = 0;
+            for (int j = 0; j < kSelectThreads / 64; ++j) tot += wcount[j];
+            if (sel) out[off + before] = n;
+            base += tot;
+            __syncthreads();
+        }
+        for (int n = kk + tid; n < nk; n += kSelectThreads) out[n] = -1;
+        if (tid == 0) block_count[(int64_t)i * sh.mq + m] = kk;
+    }
+}
+
+hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,
+                         int* head_count, hipStream_t st) {
+    hipLaunchKernelGGL(budget_kernel, dim3(sh.hq), dim3(kBudgetThreads), 0, st, sh, mass, gamma,
+                       min_blocks, head_count);
+    return hipGetLastError();
+}
+
+hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
+                         int* block_count, int* block_index, hipStream_t st) {
+    const size_t smem = (size_t)next_pow2(sh.mq) * 12;
+    if (smem > 65536) {
+        hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(select_kernel, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh, logA,
+                       head_count, block_count, block_index);
+    return hipGetLastError();
+}
+
+}  // namespace pa

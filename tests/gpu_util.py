@@ -1,0 +1,85 @@
+"""Helpers of the GPU tests: upload inputs, run the C-ABI path, fetch results."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from paper_2509_24745_amd import proxyattn as pa
+from paper_2509_24745_amd.synth import Workload, generate
+
+
+def problem_of(wl: Workload, **kw) -> pa.Problem:
+    args = dict(seq_len=wl.seq_len, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                head_dim=wl.head_dim, block_size=wl.block_size,
+                num_proxy_groups=wl.num_proxy_groups, stride=wl.stride, dtype=wl.dtype)
+    args.update(kw)
+    return pa.Problem(**args)
+
+
+def to_dev(a: np.ndarray, prob: pa.Problem) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(prob.torch_dtype).cuda()
+
+
+def to_host(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy() if t.dtype != torch.int32 else t.cpu().numpy()
+
+
+def pooled_from_workspace(prob: pa.Problem, ws: torch.Tensor):
+    qo, ko = pa.proxyattn_workspace_layout(prob)
+    npr = -(-prob.seq_len // prob.stride)
+    esz = 2 if prob.dtype == "bf16" else 4
+    count = prob.num_proxy_groups * npr * prob.head_dim
+    def view(off):
+        raw = ws[off:off + count * esz]
+        t = raw.view(prob.torch_dtype)
+        return to_host(t).reshape(prob.num_proxy_groups, npr, prob.head_dim)
+    return view(qo), view(ko)
+
+
+def run_path(prob: pa.Problem, q, k, v, gamma: float, min_budget: int = 0, lists=None):
+    """Run estimate -> select_budget -> block_sparse_prefill; return numpy results.
+
+    `lists`: optional (block_count, block_index) numpy arrays to feed the
+    attention instead of the selected lists.
+    """
+    qd, kd = to_dev(q, prob), to_dev(k, prob)
+    vd = to_dev(v, prob) if v is not None else None
+    bufs = pa.Buffers(prob)
+    pa.proxyattn_estimate(prob, qd, kd, bufs.logscore, bufs.mass, bufs.workspace)
+    pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, gamma, min_budget,
+                               bufs.head_count, bufs.block_count, bufs.block_index)
+    res = {}
+    torch.cuda.synchronize()
+    res["qg"], res["kg"] = pooled_from_workspace(prob, bufs.workspace)
+    if vd is not None:
+        bc, bi = bufs.block_count, bufs.block_index
+        if lists is not None:
+            bc = torch.from_numpy(lists[0]).cuda()
+            bi = torch.from_numpy(lists[1]).cuda()
+        pa.proxyattn_block_sparse_prefill(prob, qd, kd, vd, bc, bi, bufs.out, bufs.lse,
+                                          bufs.workspace)
+    torch.cuda.synchronize()
+    res.update(logA=to_host(bufs.logscore), mass=to_host(bufs.mass),
+               counts=to_host(bufs.head_count), block_count=to_host(bufs.block_count),
+               block_index=to_host(bufs.block_index))
+    if vd is not None:
+        res.update(out=to_host(bufs.out), lse=to_host(bufs.lse))
+    return res
+
+
+def run_attention(prob: pa.Problem, q, k, v, block_count=None, block_index=None, dense=False):
+    qd, kd, vd = to_dev(q, prob), to_dev(k, prob), to_dev(v, prob)
+    bufs = pa.Buffers(prob)
+    if dense:
+        pa.proxyattn_dense_prefill(prob, qd, kd, vd, bufs.out, bufs.lse, bufs.workspace)
+    else:
+        pa.proxyattn_block_sparse_prefill(prob, qd, kd, vd, torch.from_numpy(block_count).cuda(),
+                                          torch.from_numpy(block_index).cuda(), bufs.out, bufs.lse,
+                                          bufs.workspace)
+    torch.cuda.synchronize()
+    return to_host(bufs.out), to_host(bufs.lse)
+
+
+def inputs(wl: Workload):
+    g = generate(wl)
+    return g["q"], g["k"], g["v"]

@@ -1,0 +1,139 @@
+"""The C-ABI library on the host: it loads, exports every function the header
+declares, its problem struct matches the C compiler's layout, and argument
+validation rejects bad calls before anything reaches a GPU (these calls
+return before any HIP call, so they run without a GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "proxyattn.h")
+
+pa = pytest.importorskip("paper_2509_24745_amd.proxyattn")
+
+
+def _lib():
+    if not os.path.exists(pa.LIB_PATH):
+        pytest.skip("libproxyattn.so not built")
+    return pa.lib()
+
+
+def test_header_functions_are_all_exported():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:int|const char\*)\s+(proxyattn_\w+)\s*\(", text, re.M))
+    assert declared == set(pa.EXPORTS)
+    lib = _lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", pa.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    for name in declared:
+        assert re.search(rf"\bT {name}$", out, re.M), f"{name} not exported"
+
+
+def test_struct_layout_matches_c_compiler(tmp_path):
+    fields = [f[0] for f in pa.proxyattn_problem._fields_]
+    src = tmp_path / "layout.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "proxyattn.h"', 'int main(void){',
+             'printf("%zu\\n", sizeof(proxyattn_problem));']
+    lines += [f'printf("%zu\\n", offsetof(proxyattn_problem, {f}));' for f in fields]
+    lines += ['return 0;}']
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(pa.proxyattn_problem)
+    for f, off in zip(fields, vals[1:]):
+        assert getattr(pa.proxyattn_problem, f).offset == off, f
+
+
+def _prob(**kw):
+    base = dict(seq_len=4096, num_q_heads=32, num_kv_heads=8, head_dim=128, block_size=128,
+                num_proxy_groups=4, stride=4, dtype="bf16")
+    base.update(kw)
+    return pa.Problem(**base)
+
+
+def test_version_and_error_strings():
+    lib = _lib()
+    assert lib.proxyattn_version().decode().count(".") == 2
+    for code in range(5):
+        assert lib.proxyattn_error_string(code)
+    assert lib.proxyattn_error_string(77) == b"unknown error"
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(seq_len=-1), pa.E_INVALID),
+    (dict(num_q_heads=0), pa.E_INVALID),
+    (dict(num_q_heads=30), pa.E_UNSUPPORTED),        # 30 % 8 != 0
+    (dict(num_proxy_groups=3), pa.E_UNSUPPORTED),    # 32 % 3 != 0
+    (dict(head_dim=96), pa.E_UNSUPPORTED),
+    (dict(block_size=256), pa.E_UNSUPPORTED),
+    (dict(stride=8), pa.E_UNSUPPORTED),
+    (dict(block_size=64, stride=4, head_dim=64), None),  # b/s = 16 is fine
+    (dict(dtype="fp16"), pa.E_UNSUPPORTED),
+    (dict(seq_len=8193 * 128), pa.E_UNSUPPORTED),   # more than 8192 blocks
+    (dict(q_tok_stride=4100), pa.E_UNSUPPORTED),    # rows not 16-byte aligned
+])
+def test_problem_validation(kw, code):
+    _lib()
+    prob = _prob(**kw)
+    if code is None:
+        assert pa.proxyattn_workspace_size(prob) > 0
+        return
+    with pytest.raises(pa.ProxyAttnError) as ei:
+        pa.proxyattn_workspace_size(prob)
+    assert ei.value.code == code
+
+
+def test_bad_struct_size_and_null_problem():
+    lib = _lib()
+    p = _prob().c_struct()
+    p.struct_size = 12
+    n = ctypes.c_size_t(0)
+    assert lib.proxyattn_workspace_size(ctypes.byref(p), ctypes.byref(n)) == pa.E_INVALID
+    assert lib.proxyattn_workspace_size(None, ctypes.byref(n)) == pa.E_INVALID
+
+
+def test_workspace_size_formula_and_empty_problem():
+    _lib()
+    prob = _prob(seq_len=32768)
+    g, npr, d, mq, bp = 4, 8192, 128, 256, 32
+    expect_min = 2 * g * npr * d * 2 + g * npr * 4 + g * (mq * (mq + 1) // 2) * bp * 4 \
+        + 32 * 16 * 128 * 2 * 4 + 8 * mq * d * 128 * 2
+    ws = pa.proxyattn_workspace_size(prob)
+    assert expect_min <= ws <= expect_min + 6 * 256
+    assert pa.proxyattn_workspace_size(_prob(seq_len=0)) == 0
+
+
+def test_calls_reject_bad_arguments_before_launch():
+    lib = _lib()
+    prob = _prob()
+    p = prob.c_struct()
+    fake = 1 << 20                       # aligned, never dereferenced: calls fail first
+    ws = pa.proxyattn_workspace_size(prob)
+    # null tensor
+    assert lib.proxyattn_estimate(ctypes.byref(p), None, fake, fake, fake, fake, ws, None) \
+        == pa.E_INVALID
+    # misaligned tensor
+    assert lib.proxyattn_estimate(ctypes.byref(p), fake + 2, fake, fake, fake, fake, ws, None) \
+        == pa.E_INVALID
+    # workspace too small
+    assert lib.proxyattn_estimate(ctypes.byref(p), fake, fake, fake, fake, fake, ws - 1, None) \
+        == pa.E_WORKSPACE
+    # gamma outside (0, 1], negative minimum budget
+    for gamma, beta in ((0.0, 0), (1.5, 0), (float("nan"), 0), (0.9, -1)):
+        assert lib.proxyattn_select_budget(ctypes.byref(p), fake, fake, gamma, beta, fake, fake,
+                                           fake, None) == pa.E_INVALID
+    assert b"gamma" in lib.proxyattn_last_error() or b"min_budget" in lib.proxyattn_last_error()
+    # prefill without lists
+    assert lib.proxyattn_block_sparse_prefill(ctypes.byref(p), fake, fake, fake, None, fake, fake,
+                                              None, fake, ws, None) == pa.E_INVALID
+    # empty problem: valid no-op, nothing touched
+    p0 = _prob(seq_len=0).c_struct()
+    assert lib.proxyattn_estimate(ctypes.byref(p0), None, None, None, None, None, 0, None) == 0
+    assert lib.proxyattn_dense_prefill(ctypes.byref(p0), None, None, None, None, None, None, 0,
+                                       None) == 0
