@@ -134,8 +134,10 @@ int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
  *  block_count [Hq][Mq] int32 (out): min(head_count[i], m+1).
  *  block_index [Hq][Mq][Nk] int32 (out): for head i and block row m, the
  *      block_count[i][m] causal blocks n <= m with the highest
- *      block_logscore[g(i)][m][n] (ties to the lower n), in ascending order,
- *      then -1 up to Nk.
+ *      block_logscore[g(i)][m][n] (ties to the lower n), listed from the
+ *      highest score down, then -1 up to Nk.  In this order the lists of the
+ *      heads of one proxy group are prefixes of one another, which lets the
+ *      attention step fetch shared key/value blocks once for all of them.
  */
 int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logscore,
                             const float* lastblk_mass, float gamma, int32_t min_budget_tokens,
@@ -145,10 +147,11 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
 /*
  * Step 3: block-sparse causal attention.  For query token t in block m and
  * head i, out[t][i] = softmax_u(c * <q_t, k_u>) v_u over the keys u <= t of
- * the blocks block_index[i][m][0 .. block_count[i][m]).  Lists must be
- * ascending, unique, within 0..m, with 1 <= count <= m+1 (the lists
- * proxyattn_select_budget writes satisfy this; a row with count 0 gets
- * out = 0 and lse = -inf).
+ * the blocks block_index[i][m][0 .. block_count[i][m]).  Lists may be in any
+ * order but must hold distinct blocks within 0..m, with 1 <= count <= m+1
+ * (the lists proxyattn_select_budget writes satisfy this; a row with count 0
+ * gets out = 0 and lse = -inf; out-of-range entries are clamped, never read
+ * out of bounds).  Blocks are accumulated in list order.
  *  out: [N][Hq][d] in the problem's dtype (o strides).
  *  lse: [Hq][N] fp32 natural-log row log-sum-exp, or NULL.
  *  workspace: as for proxyattn_estimate (holds a blocked copy of V).

@@ -10,9 +10,10 @@ Agreement required (the tolerances of the north-star specification):
     P[c-1] >= gamma - window and (c == 1 or P[c-2] < gamma + window)
     (window 1e-4, shares computed in float64 from the oracle's fp32 masses).
   * block lists: per (head, block row) the symmetric difference between the
-    GPU's list and the oracle's selection at the GPU's count may hold only
-    blocks whose oracle log-score lies within `window` of the oracle's
-    K-th largest log-score (1e-4 in the log domain = 1e-4 relative in A).
+    GPU's list (as a set) and the oracle's selection at the GPU's count may
+    hold only blocks whose oracle log-score lies within `window` of the
+    oracle's K-th largest log-score (1e-4 in the log domain = 1e-4 relative
+    in A); the GPU lists blocks from the highest score down.
   * attention: max |dO| <= 2e-2 and mean |dO| <= 2e-3 against the oracle's
     attention on the GPU's own lists.
 """
@@ -77,9 +78,12 @@ def check_counts(gpu_counts, oracle_counts, oracle_cums, gamma, min_budget_token
 
 
 def check_lists(gpu_count, gpu_index, logA, counts_used, num_q_heads, rows=None,
-                report: Report | None = None, window: float = WINDOW) -> Report:
+                report: Report | None = None, window: float = WINDOW,
+                rank_order: bool = True) -> Report:
     """Verify GPU lists against the oracle's shared scores `logA` [G, Mq, Nk].
 
+    Lists are compared as sets; with `rank_order` they must also be listed
+    from the highest score down (the library's documented order).
     `counts_used`: the per-head budget the GPU used (already validated).
     """
     report = report or Report()
@@ -96,15 +100,22 @@ def check_lists(gpu_count, gpu_index, logA, counts_used, num_q_heads, rows=None,
                 kk = min(int(counts_used[i]), m + 1)
                 if int(gpu_count[i, m]) != kk:
                     raise ParityError(f"head {i} row {m}: count {int(gpu_count[i, m])} != {kk}")
-                lst = gpu_index[i, m, :kk]
+                lst_raw = gpu_index[i, m, :kk]
+                lst = np.sort(lst_raw)
                 if kk > 1 and np.any(np.diff(lst) <= 0):
-                    raise ParityError(f"head {i} row {m}: list not strictly ascending: {lst}")
+                    raise ParityError(f"head {i} row {m}: list repeats a block: {lst_raw}")
                 if kk and (lst.min() < 0 or lst.max() > m):
                     raise ParityError(f"head {i} row {m}: index out of range: {lst}")
                 if np.any(gpu_index[i, m, kk:] != -1):
                     raise ParityError(f"head {i} row {m}: padding is not -1")
                 ref = np.sort(order[:kk])
                 report.rows_checked += 1
+                if rank_order and kk > 1:
+                    # listed from the highest score down (up to near-ties)
+                    drop = np.diff(sc[lst_raw])
+                    if np.any(drop > window):
+                        raise ParityError(f"head {i} row {m}: list not in score order: "
+                                          f"{lst_raw} scores {sc[lst_raw]}")
                 if np.array_equal(lst, ref):
                     continue
                 theta = sc[order[kk - 1]]

@@ -5,6 +5,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "proxyattn.h"
@@ -30,6 +31,11 @@ static int hip_fail(hipError_t e, const char* where) {
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static int env_int(const char* name, int dflt) {
+    const char* v = getenv(name);
+    return (v && *v) ? atoi(v) : dflt;
+}
 
 // Validates the descriptor and resolves it into a Shape.
 static int resolve(const proxyattn_problem* p, Shape* sh) {
@@ -86,6 +92,10 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     s.kv_head = p->kv_head_stride ? p->kv_head_stride : d;
     s.o_tok = p->o_tok_stride ? p->o_tok_stride : (int64_t)p->num_q_heads * d;
     s.o_head = p->o_head_stride ? p->o_head_stride : d;
+    // attention work order (tuning knob; the default is the measured best on
+    // MI355X)
+    s.attn_order = env_int("PROXYATTN_ATTN_ORDER", 1);
+    s.attn_chunk_rows = env_int("PROXYATTN_ATTN_CHUNK_ROWS", 2);
     const int64_t strides[6] = {s.q_tok, s.q_head, s.kv_tok, s.kv_head, s.o_tok, s.o_head};
     for (int j = 0; j < 6; ++j) {
         if (strides[j] < 0) return fail(PROXYATTN_E_INVALID, "negative stride");
@@ -105,7 +115,7 @@ WsLayout ws_layout(const Shape& sh) {
     L.lse2 = off; off = align_up(off + (size_t)sh.g * sh.np * 4);
     L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.nchunks * sh.b * 2 * 4);
-    L.vt = off;   off = align_up(off + (size_t)sh.hkv * sh.mq * sh.d * sh.b * esz);
+    L.kvb = off;  off = align_up(off + (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz);
     L.total = off;
     return L;
 }
@@ -233,8 +243,8 @@ static int prefill_common(const proxyattn_problem* p, const void* q, const void*
     PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    PA_LAUNCH(launch_vt(sh, v, ws + L.vt, st), "v_blocked");
-    PA_LAUNCH(launch_attention(sh, dense, q, k, ws + L.vt, block_count, block_index, out, lse, st),
+    PA_LAUNCH(launch_kv_block(sh, k, v, ws + L.kvb, st), "kv_block");
+    PA_LAUNCH(launch_attention(sh, dense, q, ws + L.kvb, block_count, block_index, out, lse, st),
               "attention");
     return PROXYATTN_OK;
 }

@@ -2,23 +2,34 @@
 // paragraph) and its dense baseline (every causal block).
 //
 // Work item = (query head i, query block m): b query rows, one wave per 32
-// rows.  The item walks its list of key blocks; for each block it computes
+// rows.  The item walks its list of key blocks in sub-blocks of 64 keys; for
+// each sub-block it computes
 //   S^T = K Q^T            (32x32x16 bf16 MFMA; K from LDS, Q in registers)
 //   online softmax          (lane-local per query + one half-wave exchange)
 //   O^T += V^T P^T          (P^T straight from the S^T accumulators)
-// Each lane owns one query column of every tile, so the probabilities of
+// Each lane owns one query column of every tile, so the probabilities in
 // S^T's accumulators are already laid out as the B operand of the PV
 // product: a 32-key tile's 16 accumulator slots of lane half h cover keys
-// 8(r/4) + 4h + r%4, and the V^T operand is read with the same key order.
-// That order is baked into a blocked copy of V made once per call:
-//   vt[h][n][d][p],  p = key-in-block with bits 2 and 3 of its offset in
-//   the 32-key tile swapped,
-// so that the 8 keys a lane needs for one PV step are contiguous (one 16-byte
-// LDS read), and staging a V^T block is a contiguous 16-byte-per-thread copy.
+// 8(r/4) + 4h + r%4, and the V^T operand is read in that key order.
 //
-// K and V^T tiles of the next listed block are fetched into registers while
-// the current block is computed, then written to the other LDS buffer
-// (double buffered; single buffered when two stages do not fit in LDS).
+// A pre-pass re-blocks K and V once per call into
+//   kvb[h][n][sub] = { K rows of the sub-block (64 x d, row-major),
+//                      V^T of the sub-block (d x 64, keys permuted: bits 2
+//                      and 3 of the offset in each 32-key tile swapped) }
+// so that every sub-block is one contiguous 16*d*8-byte chunk (spread over
+// all HBM channels whatever KV head is being read), the 8 keys a lane needs
+// for one PV step are contiguous (one 16-byte LDS read), and rows past N are
+// zero.
+//
+// Pipeline (one barrier per 64-key step j; two workgroups share a CU):
+//   - sub-tiles are copied global -> LDS with global_load_lds (no staging
+//     registers); K and V^T have separate double buffers, K one step ahead:
+//     during step j the copies of K(j+2) and V(j+1) run while the wave reads
+//     K(j+1) and V(j);
+//   - the scores of step j+1 (MFMA) are interleaved instruction by
+//     instruction with the softmax of step j (VALU) in one basic block, then
+//     PV of step j runs; the row max of step j+1 closes the step, so the
+//     rare rescale branch stays out of that block.
 #include "common.h"
 #include "internal.h"
 
@@ -29,79 +40,278 @@ __device__ __forceinline__ int swap_bits23(int x) {
 }
 
 // ---------------------------------------------------------------------------
-// V -> blocked V^T.  grid (Mq, Hkv), 256 threads.  Keys >= N are zero.
+// K, V -> kvb.  grid (Mq, Hkv), 256 threads.  Rows >= N are zero.
 // ---------------------------------------------------------------------------
+constexpr int kSubKeys = 64;  // keys per attention sub-block
+
 template <typename T, int D, int B>
-__global__ __launch_bounds__(256) void vt_kernel(Shape sh, const T* __restrict__ v,
-                                                 T* __restrict__ vt) {
+__global__ __launch_bounds__(256) void kv_block_kernel(Shape sh, const T* __restrict__ k,
+                                                       const T* __restrict__ v,
+                                                       T* __restrict__ kvb) {
     constexpr int V = Vec16<T>::n;
     constexpr int LDR = D + V;
+    constexpr int KT = kSubKeys < B ? kSubKeys : B;
+    constexpr int SUB = 2 * KT * D;
     __shared__ __attribute__((aligned(16))) T tile[B * LDR];
     const int blk = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
-    const T* src = v + (int64_t)h * sh.kv_head;
+    const T* ksrc = k + (int64_t)h * sh.kv_head;
+    const T* vsrc = v + (int64_t)h * sh.kv_head;
+    T* dst = kvb + ((int64_t)h * sh.mq + blk) * (2 * B * D);
     for (int vi = tid; vi < B * D / V; vi += 256) {
         const int row = vi / (D / V), col = (vi % (D / V)) * V;
         const int tok = blk * B + row;
-        uint4 x = make_uint4(0, 0, 0, 0);
-        if (tok < sh.n) x = *reinterpret_cast<const uint4*>(src + (int64_t)tok * sh.kv_tok + col);
-        *reinterpret_cast<uint4*>(tile + row * LDR + col) = x;
+        u32x4 xk = zero_u32x4(), xv = zero_u32x4();
+        if (tok < sh.n) {
+            xk = *reinterpret_cast<const u32x4*>(ksrc + (int64_t)tok * sh.kv_tok + col);
+            xv = *reinterpret_cast<const u32x4*>(vsrc + (int64_t)tok * sh.kv_tok + col);
+        }
+        // K rows go straight to their sub-block
+        T* kd = dst + (row / KT) * SUB + (row % KT) * D + col;
+        *reinterpret_cast<u32x4*>(kd) = xk;
+        *reinterpret_cast<u32x4*>(tile + row * LDR + col) = xv;
     }
     __syncthreads();
-    T* dst = vt + ((int64_t)h * sh.mq + blk) * (D * B);
+    // V^T: row d of sub-block `sub` holds its KT keys in permuted order
     for (int ov = tid; ov < D * B / V; ov += 256) {
-        const int d = ov / (B / V), p0 = (ov % (B / V)) * V;
-        uint4 x;
-        T* xe = reinterpret_cast<T*>(&x);
+        const int sub = ov / (D * KT / V);
+        const int rem = ov % (D * KT / V);
+        const int d = rem / (KT / V), p0 = (rem % (KT / V)) * V;
+        u32x4 x = zero_u32x4();
 #pragma unroll
         for (int e = 0; e < V; ++e) {
             const int p = p0 + e;
-            const int key = (p & ~31) | swap_bits23(p & 31);
-            xe[e] = tile[key * LDR + d];
+            const int key = sub * KT + ((p & ~31) | swap_bits23(p & 31));
+            put_elem<T>(x, e, tile[key * LDR + d]);
         }
-        *reinterpret_cast<uint4*>(dst + (int64_t)d * B + p0) = x;
+        *reinterpret_cast<u32x4*>(dst + sub * SUB + KT * D + d * KT + p0) = x;
     }
 }
 
 // ---------------------------------------------------------------------------
-// attention.  grid Hq*Mq, 2B threads.
+// attention.  grid attn_grid(sh), 2B threads (B/32 waves), 2 workgroups per CU.
 // ---------------------------------------------------------------------------
 template <typename T> __device__ __forceinline__ T cvt_p(float p);
 template <> __device__ __forceinline__ bf16 cvt_p<bf16>(float p) { return (bf16)p; }
 template <> __device__ __forceinline__ float cvt_p<float>(float p) { return p; }
 
+// Slack (log2 units) by which a row max may exceed the running reference max
+// before the accumulators are rescaled.
+constexpr float kRescaleSlack = 8.f;
+
 template <typename T, int D, int B>
 struct AttnCfg {
     static constexpr int V = Vec16<T>::n;
-    static constexpr int NTH = 2 * B;          // B/32 waves
-    static constexpr int KPAD = D + V;         // padded K row (elements)
-    static constexpr int VPAD = B + V;         // padded V^T row
-    static constexpr int K_ELEMS = B * KPAD;
+    static constexpr int NTH = 2 * B;                  // B/32 waves
+    static constexpr int KT = kSubKeys < B ? kSubKeys : B;  // keys per sub-block
+    static constexpr int NSUB = B / KT;                // sub-blocks per block
+    static constexpr int NT = KT / 32;                 // 32-key tiles per sub-block
+    static constexpr int SUB = 2 * KT * D;             // elements of a kvb sub-block
+    static constexpr int KPAD = D + V;                 // padded K row in LDS (elements)
+    static constexpr int VPAD = KT + V;                // padded V^T row in LDS
+    static constexpr int K_ELEMS = KT * KPAD;
     static constexpr int V_ELEMS = D * VPAD;
     static constexpr int STAGE = K_ELEMS + V_ELEMS;
-    static constexpr int STAGES = (2 * STAGE * (int)sizeof(T) <= 160 * 1024) ? 2 : 1;
-    static constexpr int VPT = (B * D / V) / NTH;  // 16-byte vectors per thread per tile
+    static constexpr int VPT = SUB / V / NTH;          // 16-byte vectors per thread per sub-block
 };
 
+// Work item of workgroup `b`.  Workgroups are dealt to the XCDs round-robin:
+// XCD x = b % 8 sees its workgroups in slot order b / 8.
+// Order 0: longest block rows first, heads fastest.
+// Order 1 (row chunks): chunks of R consecutive block rows (longest first)
+//   x all query heads, KV heads outermost inside a chunk; chunk c runs on
+//   XCD c % 8.  Inside an XCD the query heads of one KV head on neighbouring
+//   rows are adjacent, so the K/V sub-blocks they fetch are shared through
+//   the XCD's L2; chunks dealt in turn balance the XCDs.
+// Order 2 (KV-head-major chunks): chunks of R rows x the query heads of ONE
+//   KV head, ordered KV head by KV head; chunk L runs on XCD L % 8.  At any
+//   time the whole GPU reads the K/V of about one KV head, which stays
+//   resident in the MALL.
+// Returns false for padding workgroups.
+__device__ __forceinline__ bool attn_item(const Shape& sh, int b, int* m_out, int* i_out) {
+    const int R = sh.attn_chunk_rows;
+    if (sh.attn_order == 0 || R <= 0) {
+        if (b >= sh.hq * sh.mq) return false;
+        *m_out = sh.mq - 1 - b / sh.hq;
+        *i_out = b % sh.hq;
+        return true;
+    }
+    const int x = b % kNumXcd, slot = b / kNumXcd;
+    if (sh.attn_order == 1) {
+        const int chunk_items = sh.hq * R;
+        const int c = x + kNumXcd * (slot / chunk_items);
+        const int within = slot % chunk_items;
+        const int kv = within / (R * sh.rep);
+        const int r = (within / sh.rep) % R;
+        const int m = sh.mq - 1 - (c * R + r);
+        if (m < 0) return false;
+        *m_out = m;
+        *i_out = kv * sh.rep + within % sh.rep;
+        return true;
+    }
+    const int chunk_items = sh.rep * R;
+    const int chunks_per_kv = (sh.mq + R - 1) / R;
+    const int L = x + kNumXcd * (slot / chunk_items);
+    if (L >= sh.hkv * chunks_per_kv) return false;
+    const int kv = L / chunks_per_kv, c = L % chunks_per_kv;
+    const int within = slot % chunk_items;
+    const int m = sh.mq - 1 - (c * R + within / sh.rep);
+    if (m < 0) return false;
+    *m_out = m;
+    *i_out = kv * sh.rep + within % sh.rep;
+    return true;
+}
+
+static int attn_grid(const Shape& sh) {
+    const int R = sh.attn_chunk_rows;
+    if (sh.attn_order == 0 || R <= 0) return sh.hq * sh.mq;
+    if (sh.attn_order == 1) {
+        const int chunks = (sh.mq + R - 1) / R;
+        return kNumXcd * ((chunks + kNumXcd - 1) / kNumXcd) * sh.hq * R;
+    }
+    const int chunks = sh.hkv * ((sh.mq + R - 1) / R);
+    return kNumXcd * ((chunks + kNumXcd - 1) / kNumXcd) * sh.rep * R;
+}
+
+// Direct global -> LDS copy of one kvb sub-block (K rows, then V^T rows)
+// into the padded LDS layout.  One global_load_lds_dwordx4 moves 64
+// consecutive 16-byte LDS slots (slot = lane); the padded layout has one
+// spare slot per row, which loads a harmless duplicate of the row's first
+// chunk.  Instructions are dealt to the waves round-robin; each lane's byte
+// offsets inside a sub-block are loop invariant and computed once.
+template <typename T, int D, int B>
+struct SubTileDma {
+    typedef AttnCfg<T, D, B> C;
+    static constexpr int V = C::V;
+    static constexpr int NW = C::NTH / 64;
+    static constexpr int KSR = D / V + 1;              // slots per padded K row
+    static constexpr int VSR = C::KT / V + 1;          // slots per padded V^T row
+    static constexpr int K_INS = C::KT * KSR / 64;     // wave instructions, K part
+    static constexpr int V_INS = D * VSR / 64;         // wave instructions, V^T part
+    static constexpr int KJ = (K_INS + NW - 1) / NW;   // per wave (upper bound)
+    static constexpr int VJ = (V_INS + NW - 1) / NW;
+    static_assert(C::KT * KSR % 64 == 0 && D * VSR % 64 == 0, "whole wave instructions");
+    static_assert(C::KPAD == KSR * V && C::VPAD == VSR * V, "padded pitches");
+
+    uint32_t koff[KJ], voff[VJ];   // byte offsets inside a sub-block
+    int w;
+
+    __device__ __forceinline__ SubTileDma(int w_, int lane) : w(w_) {
+#pragma unroll
+        for (int j = 0; j < KJ; ++j) {
+            const int slot = (w + j * NW) * 64 + lane;
+            const int row = slot / KSR, ch = slot % KSR;
+            koff[j] = (uint32_t)((row * D + (ch == KSR - 1 ? 0 : ch * V)) * sizeof(T));
+        }
+#pragma unroll
+        for (int j = 0; j < VJ; ++j) {
+            const int slot = (w + j * NW) * 64 + lane;
+            const int row = slot / VSR, ch = slot % VSR;
+            voff[j] = (uint32_t)((C::KT * D + row * C::KT + (ch == VSR - 1 ? 0 : ch * V)) * sizeof(T));
+        }
+    }
+    __device__ __forceinline__ void issue_k(const T* src, T* k_lds) const {
+        const char* base = reinterpret_cast<const char*>(src);
+#pragma unroll
+        for (int j = 0; j < KJ; ++j) {
+            const int ins = w + j * NW;
+            if (KJ * NW == K_INS || ins < K_INS)
+                __builtin_amdgcn_global_load_lds((const void*)(base + koff[j]),
+                                                 (void*)(k_lds + ins * 64 * V), 16, 0, 0);
+        }
+    }
+    __device__ __forceinline__ void issue_v(const T* src, T* v_lds) const {
+        const char* base = reinterpret_cast<const char*>(src);
+#pragma unroll
+        for (int j = 0; j < VJ; ++j) {
+            const int ins = w + j * NW;
+            if (VJ * NW == V_INS || ins < V_INS)
+                __builtin_amdgcn_global_load_lds((const void*)(base + voff[j]),
+                                                 (void*)(v_lds + ins * 64 * V), 16, 0, 0);
+        }
+    }
+};
+
+// Causal / ragged mask of one 64-key sub-tile: keys past `lim` (offset of
+// the last visible key inside the sub-tile) become -inf.  A key's offset is
+// 32 kt + 8 (r/4) + (r%4) + 4 h; the compile-time part is compared with the
+// per-lane limit lim - 4h.
+template <int NT>
+__device__ __forceinline__ void mask_tail(f32x16* s, int lim, int h) {
+    const int lim_h = lim - 4 * h;
+#pragma unroll
+    for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            s[kt][r] = (32 * kt + 8 * (r >> 2) + (r & 3) <= lim_h) ? s[kt][r] : kNegInf;
+}
+
+// Max of a lane's raw scores over the sub-tile, then over both wave halves
+// (four independent chains instead of one serial one).
+template <int NT>
+__device__ __forceinline__ float tile_max(const f32x16* s) {
+    float c[4] = {kNegInf, kNegInf, kNegInf, kNegInf};
+#pragma unroll
+    for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) c[(r >> 1) & 3] = fmaxf(c[(r >> 1) & 3], fmaxf(s[kt][r], s[kt][r + 1]));
+    const float mx = fmaxf(fmaxf(c[0], c[1]), fmaxf(c[2], c[3]));
+    return fmaxf(mx, swap_halves(mx));
+}
+
+// Sum of the probabilities a lane feeds to the PV product.  bf16: two per
+// v_dot2_f32_bf16 (the sum then matches the rounded P the MFMA consumes).
+template <typename T, int NT>
+__device__ __forceinline__ float prob_sum(const typename FragOf<T>::type (*pf)[2]);
+
+template <>
+__device__ __forceinline__ float prob_sum<bf16, 2>(const bf16x8 (*pf)[2]) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const bf16x2 pr = {pf[kt][e][2 * j], pf[kt][e][2 * j + 1]};
+                acc[j] = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc[j], false);
+            }
+    return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
+template <>
+__device__ __forceinline__ float prob_sum<float, 2>(const f32x8 (*pf)[2]) {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[j & 3] += pf[kt][e][j];
+    return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
 template <typename T, int D, int B, bool DENSE>
-__global__ __launch_bounds__(2 * B, 1) void attn_kernel(Shape sh, const T* __restrict__ q,
-                                                        const T* __restrict__ k,
-                                                        const T* __restrict__ vt,
+__global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __restrict__ q,
+                                                        const T* __restrict__ kvb,
                                                         const int* __restrict__ block_count,
                                                         const int* __restrict__ block_index,
                                                         T* __restrict__ out,
                                                         float* __restrict__ lse) {
     typedef AttnCfg<T, D, B> C;
     typedef typename FragOf<T>::type Frag;
-    constexpr int NT = B / 32;   // key tiles per block
+    typedef SubTileDma<T, D, B> Dma;
+    constexpr int NT = C::NT;
     constexpr int DT = D / 32;   // output tiles along d
     constexpr int KS = D / 16;   // k steps of Q K^T
-    constexpr int V = C::V;
-    __shared__ __attribute__((aligned(16))) T smem[C::STAGES * C::STAGE];
+    static_assert(NT == 2, "64-key sub-tiles");
+    __shared__ __attribute__((aligned(16))) T ks_buf[2][C::K_ELEMS];
+    __shared__ __attribute__((aligned(16))) T vs_buf[2][C::V_ELEMS];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
-    const int item = blockIdx.x;
-    const int m = sh.mq - 1 - item / sh.hq;     // longest rows first
-    const int i = item % sh.hq;
+    int m, i;
+    if (!attn_item(sh, blockIdx.x, &m, &i)) return;
     const int kvh = i / sh.rep;
     const int n_tok = sh.n;
     // counts and indices are clamped to the causal range, so malformed caller
@@ -110,6 +320,7 @@ __global__ __launch_bounds__(2 * B, 1) void attn_kernel(Shape sh, const T* __res
     const int* list = DENSE ? nullptr : block_index + ((int64_t)i * sh.mq + m) * sh.mq;
     const int qtok = m * B + 32 * w + lc;
     const bool qvalid = qtok < n_tok;
+    const int qlim = min(qtok, n_tok - 1);   // last key this row may see
 
     if (cnt <= 0) {
         if (qvalid) {
@@ -127,32 +338,30 @@ __global__ __launch_bounds__(2 * B, 1) void attn_kernel(Shape sh, const T* __res
         for (int ks = 0; ks < KS; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
     }
 
-    const T* kbase = k + (int64_t)kvh * sh.kv_head;
-    const T* vbase = vt + (int64_t)kvh * sh.mq * (D * B);
-    u32x4 kreg[C::VPT], vreg[C::VPT];
-    auto fetch = [&](int nb) {
-        const T* kb = kbase + (int64_t)nb * B * sh.kv_tok;
-        const T* vb = vbase + (int64_t)nb * (D * B);
-#pragma unroll
-        for (int c = 0; c < C::VPT; ++c) {
-            const int vi = tid + c * C::NTH;
-            const int row = vi / (D / V), col = (vi % (D / V)) * V;
-            kreg[c] = (nb * B + row < n_tok)
-                          ? *reinterpret_cast<const u32x4*>(kb + (int64_t)row * sh.kv_tok + col)
-                          : zero_u32x4();
-            vreg[c] = *reinterpret_cast<const u32x4*>(vb + (int64_t)vi * V);
+    const T* kvbase = kvb + (int64_t)kvh * sh.mq * (2 * B * D);
+    // step j = sub-block (j % NSUB) of listed block (j / NSUB).  List entries
+    // arrive 64 at a time, one per lane, through a vector load, and are picked
+    // with v_readlane: no scalar-memory load in the loop, whose out-of-order
+    // return would force every LDS wait to drain completely.
+    int lst_base = -64, lst = 0;
+    auto block_of = [&](int it) -> int {
+        if (DENSE) return it;
+        const int c0 = it & ~63;
+        if (c0 != lst_base) {
+            lst_base = c0;
+            lst = (c0 + lane < cnt) ? list[c0 + lane] : 0;
         }
+        return min(max(__builtin_amdgcn_readlane(lst, it & 63), 0), m);
     };
-    auto stash = [&](int buf) {
-        T* ks_ = smem + buf * C::STAGE;
-        T* vs_ = ks_ + C::K_ELEMS;
+    auto sub_src = [&](int nb, int sub) { return kvbase + (int64_t)nb * (2 * B * D) + sub * C::SUB; };
+    auto needs_mask = [&](int nb) { return nb == m || (nb + 1) * B > n_tok; };
+    auto qk = [&](f32x16* acc, const T* kt_) {
 #pragma unroll
-        for (int c = 0; c < C::VPT; ++c) {
-            const int vi = tid + c * C::NTH;
-            const int row = vi / (D / V), col = (vi % (D / V)) * V;
-            *reinterpret_cast<u32x4*>(ks_ + row * C::KPAD + col) = kreg[c];
-            const int vrow = vi / (B / V), vcol = (vi % (B / V)) * V;
-            *reinterpret_cast<u32x4*>(vs_ + vrow * C::VPAD + vcol) = vreg[c];
+        for (int kt = 0; kt < NT; ++kt) {
+            acc[kt] = zero16();
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                mma(acc[kt], load_frag<T>(kt_ + (32 * kt + lc) * C::KPAD + 16 * ks + 8 * h), qf[ks]);
         }
     };
 
@@ -161,78 +370,100 @@ __global__ __launch_bounds__(2 * B, 1) void attn_kernel(Shape sh, const T* __res
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = zero16();
 
-    int n_cur = DENSE ? 0 : min(max(list[0], 0), m);
-    fetch(n_cur);
-    stash(0);
+    const int steps = cnt * C::NSUB;
+    auto nb_of_step = [&](int j, int nb_prev) {
+        return (j % C::NSUB == 0) ? block_of(j / C::NSUB) : nb_prev;
+    };
+    // prologue: K of steps 0 and 1, V of step 0; scores and max of step 0
+    int nb0 = block_of(0);
+    int nb1 = steps > 1 ? nb_of_step(1, nb0) : nb0;
+    const Dma dma(w, lane);
+    dma.issue_k(sub_src(nb0, 0), ks_buf[0]);
+    dma.issue_v(sub_src(nb0, 0), vs_buf[0]);
+    if (steps > 1) dma.issue_k(sub_src(nb1, 1 % C::NSUB), ks_buf[1]);
     __syncthreads();
-    for (int it = 0; it < cnt; ++it) {
-        const int buf = (C::STAGES == 2) ? (it & 1) : 0;
-        int n_next = -1;
-        if (it + 1 < cnt) {
-            n_next = DENSE ? it + 1 : min(max(list[it + 1], 0), m);
-            fetch(n_next);
-        }
-        const T* ks_ = smem + buf * C::STAGE;
-        const T* vs_ = ks_ + C::K_ELEMS;
+    f32x16 s_cur[NT];
+    qk(s_cur, ks_buf[0]);
+    if (needs_mask(nb0)) mask_tail<NT>(s_cur, qlim - nb0 * B, h);
+    float mx = tile_max<NT>(s_cur) * sh.scale2;
 
-        f32x16 s[NT];
-#pragma unroll
-        for (int kt = 0; kt < NT; ++kt) {
-            s[kt] = zero16();
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                mma(s[kt], load_frag<T>(ks_ + (32 * kt + lc) * C::KPAD + 16 * ks + 8 * h), qf[ks]);
+    // One 64-key step.  `sc` holds the scores of step st, `sn` receives those
+    // of step st+1 (two distinct register sets, used alternately, so the next
+    // scores never wait for the current softmax to free its registers).
+    auto step = [&](f32x16* sc, f32x16* sn, int st) {
+        // K(st+1) and V(st) have landed; every wave is done with step st-1,
+        // whose slots (K(st), V(st-1)) the next copies overwrite
+        __syncthreads();
+        int nb2 = nb1;
+        if (st + 2 < steps) {
+            nb2 = nb_of_step(st + 2, nb1);
+            dma.issue_k(sub_src(nb2, (st + 2) % C::NSUB), ks_buf[st & 1]);
         }
-        const bool need_mask = (n_cur == m) || ((n_cur + 1) * B > n_tok);
-        float mx = kNegInf;
+        if (st + 1 < steps) dma.issue_v(sub_src(nb1, (st + 1) % C::NSUB), vs_buf[(st + 1) & 1]);
+
+        // lazy rescaling: the reference max moves only when some row's max
+        // exceeds it by more than kRescaleSlack (probabilities stay < 2^8)
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack)) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = (m_run == kNegInf) ? 0.f : fast_exp2(m_run - m_new);
+            l_run *= alpha;
 #pragma unroll
-        for (int kt = 0; kt < NT; ++kt) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float x = s[kt][r] * sh.scale2;
-                if (need_mask) {
-                    const int key = n_cur * B + 32 * kt + c_row(r, h);
-                    if (key > qtok || key >= n_tok) x = kNegInf;
-                }
-                s[kt][r] = x;
-                mx = fmaxf(mx, x);
-            }
+            for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+            m_run = m_new;
         }
-        mx = fmaxf(mx, swap_halves(mx));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-        const float alpha = exp2f(m_run - m_use);
-        float psum = 0.f;
+        // a row whose keys so far are all masked keeps m_run = -inf: its
+        // probabilities are exp2(-inf) = 0
+        const float neg_m = (m_run == kNegInf) ? 0.f : -m_run;
+
+        // --- one basic block: scores of step st+1 (MFMA) interleaved with the
+        // softmax of step st (VALU), then PV of step st (MFMA).  On the last
+        // step the scores are computed from a stale slot and discarded.
+        qk(sn, ks_buf[(st + 1) & 1]);
         Frag pf[NT][2];
 #pragma unroll
-        for (int kt = 0; kt < NT; ++kt) {
+        for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = exp2f(s[kt][r] - m_use);
-                psum += p;
-                pf[kt][r >> 3][r & 7] = cvt_p<T>(p);
-            }
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
+            for (int r = 0; r < 16; ++r)
+                pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
+        l_run += prob_sum<T, NT>(pf);
+        const T* vt_ = vs_buf[st & 1];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-            for (int kt = 0; kt < NT; ++kt) {
+            for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
                 for (int e = 0; e < 2; ++e)
-                    mma(o[dt], load_frag<T>(vs_ + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h),
+                    mma(o[dt], load_frag<T>(vt_ + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h),
                         pf[kt][e]);
+        if constexpr (sizeof(T) == 2) {
+            // LDS fragment reads run two ahead of the MFMAs that use them;
+            // 16 x (QK MFMA, read, 5 softmax VALU), then 16 x (PV MFMA, read,
+            // 2 VALU)
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+            for (int g = 0; g < NT * KS; ++g) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x402, 5, 0);
+            }
+#pragma unroll
+            for (int g = 0; g < DT * NT * 2; ++g) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x402, 2, 0);
             }
         }
-        if (it + 1 < cnt) {
-            if (C::STAGES == 1) __syncthreads();
-            stash(C::STAGES == 2 ? (buf ^ 1) : 0);
-        }
-        __syncthreads();
-        n_cur = n_next;
+        // --- mask and max of step st+1
+        if (st + 1 < steps && needs_mask(nb1))
+            mask_tail<NT>(sn, qlim - nb1 * B - ((st + 1) % C::NSUB) * C::KT, h);
+        mx = tile_max<NT>(sn) * sh.scale2;
+        nb0 = nb1;
+        nb1 = nb2;
+    };
+    f32x16 s_alt[NT];
+    for (int st = 0; st < steps; st += 2) {
+        step(s_cur, s_alt, st);
+        if (st + 1 < steps) step(s_alt, s_cur, st + 1);
     }
 
     const float l_tot = l_run + swap_halves(l_run);
@@ -262,47 +493,47 @@ __global__ __launch_bounds__(2 * B, 1) void attn_kernel(Shape sh, const T* __res
 // launchers
 // ---------------------------------------------------------------------------
 template <typename T, int D, int B>
-static hipError_t vt_t(const Shape& sh, const void* v, void* vt, hipStream_t st) {
-    hipLaunchKernelGGL((vt_kernel<T, D, B>), dim3(sh.mq, sh.hkv), dim3(256), 0, st, sh,
-                       (const T*)v, (T*)vt);
+static hipError_t kvb_t(const Shape& sh, const void* k, const void* v, void* kvb, hipStream_t st) {
+    hipLaunchKernelGGL((kv_block_kernel<T, D, B>), dim3(sh.mq, sh.hkv), dim3(256), 0, st, sh,
+                       (const T*)k, (const T*)v, (T*)kvb);
     return hipGetLastError();
 }
 
-hipError_t launch_vt(const Shape& sh, const void* v, void* vt, hipStream_t st) {
+hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb,
+                           hipStream_t st) {
     if (sh.dtype == 0) {
-        if (sh.d == 64) return sh.b == 64 ? vt_t<bf16, 64, 64>(sh, v, vt, st) : vt_t<bf16, 64, 128>(sh, v, vt, st);
-        return sh.b == 64 ? vt_t<bf16, 128, 64>(sh, v, vt, st) : vt_t<bf16, 128, 128>(sh, v, vt, st);
+        if (sh.d == 64) return sh.b == 64 ? kvb_t<bf16, 64, 64>(sh, k, v, kvb, st) : kvb_t<bf16, 64, 128>(sh, k, v, kvb, st);
+        return sh.b == 64 ? kvb_t<bf16, 128, 64>(sh, k, v, kvb, st) : kvb_t<bf16, 128, 128>(sh, k, v, kvb, st);
     }
-    if (sh.d == 64) return sh.b == 64 ? vt_t<float, 64, 64>(sh, v, vt, st) : vt_t<float, 64, 128>(sh, v, vt, st);
-    return sh.b == 64 ? vt_t<float, 128, 64>(sh, v, vt, st) : vt_t<float, 128, 128>(sh, v, vt, st);
+    if (sh.d == 64) return sh.b == 64 ? kvb_t<float, 64, 64>(sh, k, v, kvb, st) : kvb_t<float, 64, 128>(sh, k, v, kvb, st);
+    return sh.b == 64 ? kvb_t<float, 128, 64>(sh, k, v, kvb, st) : kvb_t<float, 128, 128>(sh, k, v, kvb, st);
 }
 
 template <typename T, int D, int B>
-static hipError_t attn_t(const Shape& sh, bool dense, const void* q, const void* k, const void* vt,
+static hipError_t attn_t(const Shape& sh, bool dense, const void* q, const void* kvb,
                          const int* bc, const int* bi, void* out, float* lse, hipStream_t st) {
-    const dim3 grid((unsigned)(sh.hq * sh.mq));
+    const dim3 grid((unsigned)attn_grid(sh));
     if (dense)
-        hipLaunchKernelGGL((attn_kernel<T, D, B, true>), grid, dim3(2 * B), 0, st, sh, (const T*)q,
-                           (const T*)k, (const T*)vt, bc, bi, (T*)out, lse);
+        hipLaunchKernelGGL((attn_kernel<T, D, B, true>), grid, dim3(2 * B), 0, st, sh,
+                           (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse);
     else
-        hipLaunchKernelGGL((attn_kernel<T, D, B, false>), grid, dim3(2 * B), 0, st, sh, (const T*)q,
-                           (const T*)k, (const T*)vt, bc, bi, (T*)out, lse);
+        hipLaunchKernelGGL((attn_kernel<T, D, B, false>), grid, dim3(2 * B), 0, st, sh,
+                           (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse);
     return hipGetLastError();
 }
 
-hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* k,
-                            const void* vt, const int* bc, const int* bi, void* out, float* lse,
-                            hipStream_t st) {
+hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* kvb,
+                            const int* bc, const int* bi, void* out, float* lse, hipStream_t st) {
     if (sh.dtype == 0) {
-        if (sh.d == 64) return sh.b == 64 ? attn_t<bf16, 64, 64>(sh, dense, q, k, vt, bc, bi, out, lse, st)
-                                          : attn_t<bf16, 64, 128>(sh, dense, q, k, vt, bc, bi, out, lse, st);
-        return sh.b == 64 ? attn_t<bf16, 128, 64>(sh, dense, q, k, vt, bc, bi, out, lse, st)
-                          : attn_t<bf16, 128, 128>(sh, dense, q, k, vt, bc, bi, out, lse, st);
+        if (sh.d == 64) return sh.b == 64 ? attn_t<bf16, 64, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
+                                          : attn_t<bf16, 64, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
+        return sh.b == 64 ? attn_t<bf16, 128, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
+                          : attn_t<bf16, 128, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
     }
-    if (sh.d == 64) return sh.b == 64 ? attn_t<float, 64, 64>(sh, dense, q, k, vt, bc, bi, out, lse, st)
-                                      : attn_t<float, 64, 128>(sh, dense, q, k, vt, bc, bi, out, lse, st);
-    return sh.b == 64 ? attn_t<float, 128, 64>(sh, dense, q, k, vt, bc, bi, out, lse, st)
-                      : attn_t<float, 128, 128>(sh, dense, q, k, vt, bc, bi, out, lse, st);
+    if (sh.d == 64) return sh.b == 64 ? attn_t<float, 64, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
+                                      : attn_t<float, 64, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
+    return sh.b == 64 ? attn_t<float, 128, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
+                      : attn_t<float, 128, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
 }
 
 }  // namespace pa

@@ -30,6 +30,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // defeats scalar replacement and ends up on the stack)
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Element e of a 16-byte vector holding 16/sizeof(T) values of T.
+template <typename T> __device__ __forceinline__ void put_elem(u32x4& x, int e, T v);
+template <> __device__ __forceinline__ void put_elem<float>(u32x4& x, int e, float v) {
+    x[e] = __float_as_uint(v);
+}
+template <> __device__ __forceinline__ void put_elem<__bf16>(u32x4& x, int e, __bf16 v) {
+    const uint32_t b = __builtin_bit_cast(uint16_t, v);
+    x[e >> 1] |= (e & 1) ? (b << 16) : b;
+}
+
 __device__ __forceinline__ u32x4 zero_u32x4() {
     u32x4 z = {0u, 0u, 0u, 0u};
     return z;
@@ -96,6 +106,11 @@ template <> __device__ __forceinline__ float to_f32<bf16>(bf16 x) { return bf16_
 template <typename T> __device__ __forceinline__ T from_f32_rne(float x);
 template <> __device__ __forceinline__ float from_f32_rne<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32_rne<bf16>(float x) { return f32_to_bf16_rne(x); }
+
+// 2^x on the hardware transcendental unit (v_exp_f32, ~1 ulp; no denormal
+// range fix-up, which the softmax does not need).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
 // Value held by lane (l ^ 32): exchange between the two wave halves.
 __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }

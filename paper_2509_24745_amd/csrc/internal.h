@@ -28,7 +28,14 @@ struct Shape {
     float scale2; // c * log2(e)
     float inv_gsize;  // fl32(1 / |G|)
     int64_t q_tok, q_head, kv_tok, kv_head, o_tok, o_head;  // element strides
+    // attention work order (see attn_item): 0 plain, 1 row chunks, 2
+    // KV-head-major chunks; rows per chunk
+    int attn_order;
+    int attn_chunk_rows;
 };
+
+// Number of XCDs workgroups are dealt to round-robin on MI355X.
+constexpr int kNumXcd = 8;
 
 // Keys per chunk of the last-block mass kernels (a multiple of every block size).
 constexpr int kMassChunk = 2048;
@@ -40,7 +47,7 @@ struct WsLayout {
     size_t rbm;      // per-(row, key block) max of the scaled proxy logits,
                      // [G][Mq(Mq+1)/2][b'] fp32 (lower-triangular block pairs)
     size_t part;     // last-block partial (max, sum) [Hq][nchunks][b][2] fp32
-    size_t vt;       // blocked, transposed V [Hkv][Mq][d][b] (problem dtype)
+    size_t kvb;      // re-blocked K and V^T [Hkv][Mq][2 b d] (problem dtype)
     size_t total;
 };
 
@@ -58,9 +65,10 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
                          int* block_count, int* block_index, hipStream_t st);
-hipError_t launch_vt(const Shape& sh, const void* v, void* vt, hipStream_t st);
-hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* k,
-                            const void* vt, const int* block_count, const int* block_index,
-                            void* out, float* lse, hipStream_t st);
+hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb,
+                           hipStream_t st);
+hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* kvb,
+                            const int* block_count, const int* block_index, void* out, float* lse,
+                            hipStream_t st);
 
 }  // namespace pa

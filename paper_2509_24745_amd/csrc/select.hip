@@ -8,9 +8,12 @@
 //   gamma >= 1), then raised to the minimum budget and capped at Nk.
 // select: one workgroup per (proxy group, block row m).  The m+1 causal
 //   candidates are sorted by (score descending, index ascending) as 64-bit
-//   keys in LDS; every head of the group keeps the candidates whose rank is
-//   below min(count_i, m+1), compacted in ascending block order with
-//   wavefront ballots, and pads its row with -1.
+//   keys in LDS (bitonic); every head of the group lists the first
+//   min(count_i, m+1) of them in that rank order and pads its row with -1.
+//   Rank order makes the lists of a group's heads prefixes of one another,
+//   so the attention workgroups of those heads, which run side by side on
+//   one XCD, fetch the same K/V blocks in the same order and share them
+//   through the L2.
 #include "common.h"
 #include "internal.h"
 
@@ -113,7 +116,7 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(Shape sh,
 }
 
 // ---------------------------------------------------------------------------
-// select: grid (Mq, G), 256 threads, dynamic LDS = P * 12 bytes
+// select: grid (Mq, G), 256 threads, dynamic LDS = P * 8 bytes
 // ---------------------------------------------------------------------------
 constexpr int kSelectThreads = 256;
 
@@ -123,14 +126,11 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
                                                                 int* __restrict__ block_count,
                                                                 int* __restrict__ block_index) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-    __shared__ int wcount[kSelectThreads / 64];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x;
     const int m = blockIdx.x, g = blockIdx.y, nk = sh.mq;
     const int ncand = m + 1;
     const int P = next_pow2(ncand);
-    const int Pmax = next_pow2(nk);
     uint64_t* key = reinterpret_cast<uint64_t*>(smem_raw);
-    int* rank = reinterpret_cast<int*>(smem_raw + (size_t)Pmax * 8);
     const float* srow = logA + ((int64_t)g * sh.mq + m) * nk;
     // key: (order of -score) << 32 | index  -> ascending = score desc, index asc
     for (int n = tid; n < P; n += kSelectThreads) {
@@ -140,28 +140,14 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     }
     __syncthreads();
     bitonic_sort_asc<uint64_t>(key, P, tid, kSelectThreads);
-    for (int p = tid; p < ncand; p += kSelectThreads) rank[(int)(key[p] & 0xffffffffu)] = p;
-    __syncthreads();
+    // the sorted keys are the candidates in rank order: a head's list is the
+    // first min(count, m+1) of them (lists of one group are prefixes of
+    // each other)
     for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
         const int kk = min(head_count[i], ncand);
         int* out = block_index + ((int64_t)i * sh.mq + m) * nk;
-        int base = 0;
-        for (int c0 = 0; c0 < ncand; c0 += kSelectThreads) {
-            const int n = c0 + tid;
-            const bool sel = n < ncand && rank[n] < kk;
-            const uint64_t bal = __ballot(sel);
-            const int before = __popcll(bal & ((1ull << lane) - 1ull));
-            if (lane == 0) wcount[w] = __popcll(bal);
-            __syncthreads();
-            int off = base;
-            for (int j = 0; j < w; ++j) off += wcount[j];
-            int tot = 0;
-            for (int j = 0; j < kSelectThreads / 64; ++j) tot += wcount[j];
-            if (sel) out[off + before] = n;
-            base += tot;
-            __syncthreads();
-        }
-        for (int n = kk + tid; n < nk; n += kSelectThreads) out[n] = -1;
+        for (int p = tid; p < nk; p += kSelectThreads)
+            out[p] = p < kk ? (int)(key[p] & 0xffffffffu) : -1;
         if (tid == 0) block_count[(int64_t)i * sh.mq + m] = kk;
     }
 }
@@ -175,7 +161,7 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
 
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
                          int* block_count, int* block_index, hipStream_t st) {
-    const size_t smem = (size_t)next_pow2(sh.mq) * 12;
+    const size_t smem = (size_t)next_pow2(sh.mq) * 8;
     if (smem > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);

@@ -11,10 +11,15 @@ Bars (spec tolerances, see oracle/check.py):
     only through check_lists, which judges the lists on oracle scores;
   * last-block masses: relative 1e-4 of the row total (fp32 sums of up to
     N terms in different orders);
-  * budgets and lists: identical except threshold-ambiguous cases (window
-    1e-4), which are counted and reported;
+  * budgets and lists: identical sets except threshold-ambiguous cases
+    (window 1e-4), which are counted and reported; lists run from the
+    highest score down;
   * attention: max|dO| <= 2e-2, mean|dO| <= 2e-3 against the oracle's
-    attention on the GPU's own lists; lse |d| <= 1e-3.
+    attention on the GPU's own lists;
+  * lse (no spec bar; derived): bf16 problems normalise with the sum
+    of the bf16-rounded probabilities the PV product consumes, each within
+    2^-8 relative of the exact value, so |dlse| <= ln(1 + 2^-8) = 3.9e-3
+    (reached when one key dominates a row); LSE_TOL = 4e-3.
 """
 import math
 
@@ -31,7 +36,7 @@ pytestmark = pytest.mark.gpu
 
 LOGA_TOL = 2e-4
 MASS_RTOL = 1e-4
-LSE_TOL = 1e-3
+LSE_TOL = 4e-3
 
 
 def _gpu():
@@ -124,15 +129,23 @@ def test_min_budget_and_full_budget():
     gpu = U.run_path(prob, q, k, v, wl.gamma, wl.min_budget_tokens)
     assert np.all(gpu["counts"] >= 16)
     _compare(wl, q, k, v, gpu, _oracle(wl, q, k))
-    # gamma = 1: every head keeps every causal block, and the sparse kernel on
-    # the full lists reproduces the dense kernel bit for bit
+    # gamma = 1: every head keeps every causal block; the attention on those
+    # (score-ordered) lists matches the dense kernel to rounding, and the
+    # sparse kernel on ascending full lists reproduces it bit for bit
     full = U.run_path(prob, q, k, v, 1.0)
     mq = prob.num_blocks
     assert np.all(full["counts"] == mq)
     assert np.all(full["block_count"] == np.arange(1, mq + 1)[None, :])
+    for i in range(wl.num_q_heads):
+        for m in range(mq):
+            assert np.array_equal(np.sort(full["block_index"][i, m, :m + 1]), np.arange(m + 1))
     dense_out, dense_lse = U.run_attention(prob, q, k, v, dense=True)
-    assert np.array_equal(full["out"], dense_out)
-    assert np.array_equal(full["lse"], dense_lse)
+    rep = C.check_attention(full["out"], dense_out)
+    assert float(np.max(np.abs(full["lse"] - dense_lse))) <= LSE_TOL
+    fbc, fbi = O.full_causal_lists(wl.seq_len, wl.num_q_heads, wl.block_size)
+    asc_out, asc_lse = U.run_attention(prob, q, k, v, fbc, fbi)
+    assert np.array_equal(asc_out, dense_out)
+    assert np.array_equal(asc_lse, dense_lse)
 
 
 def test_attention_random_lists_and_dense():
@@ -186,7 +199,12 @@ def test_select_budget_on_oracle_scores_is_exact():
                   counts, wl.num_q_heads, report=rep)
     assert rep.ambiguous_rows == 0 or len(rep.ambiguous_heads) > 0
     if not rep.ambiguous_heads:
-        assert np.array_equal(bufs.block_index.cpu().numpy(), orc["block_index"])
+        # same sets as the oracle's (which lists them ascending)
+        got = bufs.block_index.cpu().numpy()
+        got_sorted = np.where(got >= 0, got, np.iinfo(np.int32).max)
+        got_sorted = np.sort(got_sorted, axis=-1)
+        got_sorted[got_sorted == np.iinfo(np.int32).max] = -1
+        assert np.array_equal(got_sorted, orc["block_index"])
 
 
 def test_head_major_strided_layout():
