@@ -44,8 +44,11 @@ def parse():
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-rows", type=int, default=8,
+    ap.add_argument("--cpu-sample-rows", type=int, default=24,
                     help="block rows of the oracle sample (all heads)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (scales the FETCH_SIZE / "
+                         "WRITE_SIZE counters) and exit")
     return ap.parse_args()
 
 
@@ -91,6 +94,23 @@ def cpu_baseline(wl, q, k, v, sample_rows: int):
     }
 
 
+def measured_traffic():
+    """HBM bytes per sparse attention launch from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE runs (copy-calibrated), or None when the kernel
+    source has changed since they were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "attn_traffic.json")
+    src = os.path.join(ROOT, "paper_2509_24745_amd", "csrc", "attention.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if rec.get("attention_hip_sha256") != sha:
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -98,6 +118,16 @@ def main():
                                    "by heads across GPUs only by design)"}))
         sys.exit(2)
     import torch
+    if args.calibrate_copy:
+        n = 1 << 30
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        a.fill_(1)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n}))
+        return
     from paper_2509_24745_amd import proxyattn as pa
     from paper_2509_24745_amd.synth import WORKLOADS, generate
 
@@ -216,9 +246,12 @@ def main():
         if t_dense else None,
         "dense_mfma_frac": round(4.0 * b * b * d * hq * mq * (mq + 1) / 2 / (t_dense * 1e-3)
                                  / 1e12 / peak, 4) if t_dense else None,
+        "computed_blocks": total_blocks,
         "roofline": {"kernel": "attn_kernel (block-sparse prefill call)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None},
+                     "frac": round(achieved / peak, 4),
+                     "traffic": measured_traffic() if wl.name == "llama3_8b_n131072" and
+                     wl.gamma == 0.95 and wl.structure.noise == 0.3 else None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
