@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=24,
                     help="block rows of the oracle sample (all heads)")
+    ap.add_argument("--sweep", choices=["gamma_sigma_128k", "llama_32k", "qwen_64k",
+                                         "llama_256k_layer"], default=None,
+                    help="print one JSON line per point of a workload sweep instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (scales the FETCH_SIZE / "
                          "WRITE_SIZE counters) and exit")
@@ -111,6 +114,148 @@ def measured_traffic():
     return rec["fetch_bytes"] + rec["write_bytes"]
 
 
+def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = True,
+            inputs=None):
+    """Time `steps` whole-path steps of workload `wl` (inputs resident in HBM).
+
+    Returns a dict of timings and derived figures; `inputs` may pass
+    already-uploaded (q, k, v) device tensors of the same shape.
+    """
+    import torch
+    from paper_2509_24745_amd import proxyattn as pa
+    from paper_2509_24745_amd.synth import generate
+
+    prob = pa.Problem(seq_len=wl.seq_len, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                      head_dim=wl.head_dim, block_size=wl.block_size,
+                      num_proxy_groups=wl.num_proxy_groups, stride=wl.stride, dtype=wl.dtype)
+    host = None
+    if inputs is None:
+        print(f"[bench] generating {wl.name} N={wl.seq_len} gamma={wl.gamma} "
+              f"sigma={wl.structure.noise} G={wl.num_proxy_groups}", file=sys.stderr, flush=True)
+        t = time.time()
+        host = generate(wl)
+        print(f"[bench] generated in {time.time() - t:.1f}s", file=sys.stderr, flush=True)
+        dt = prob.torch_dtype
+        inputs = tuple(torch.from_numpy(host[x]).to(dt).cuda() for x in ("q", "k", "v"))
+    q, k, v = inputs
+    bufs = pa.Buffers(prob)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, stream)
+        if ev: ev[1].record(stream)
+        pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma, wl.min_budget_tokens,
+                                   bufs.head_count, bufs.block_count, bufs.block_index, stream)
+        if ev: ev[2].record(stream)
+        pa.proxyattn_block_sparse_prefill(prob, q, k, v, bufs.block_count, bufs.block_index,
+                                          bufs.out, bufs.lse, bufs.workspace, stream)
+        if ev: ev[3].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(steps):
+        step(evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop) / steps
+    t_est = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    t_sel = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    print(f"[bench] {wl.name}: {ms_total:.3f} ms/step (est {t_est:.3f}, sel {t_sel:.3f}, "
+          f"attn {t_attn:.3f})", file=sys.stderr, flush=True)
+
+    mq, hq, d, b, n = prob.num_blocks, prob.num_q_heads, prob.head_dim, prob.block_size, prob.seq_len
+    total_blocks = int(bufs.block_count.sum().item())
+    counts = bufs.head_count.cpu().numpy()
+    causal_blocks = hq * mq * (mq + 1) // 2
+    f_dense = 4.0 * hq * d * n * (n + 1) / 2          # dense-equivalent causal flops
+    f_attn = 4.0 * b * b * d * total_blocks            # flops the sparse kernel computes
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    achieved = f_attn / (t_attn * 1e-3) / 1e12
+    t_dense = None
+    if with_dense:
+        de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        dense_out = torch.empty_like(bufs.out)
+        pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
+        torch.cuda.synchronize()
+        de[0].record(stream)
+        for _ in range(dense_steps):
+            pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
+        de[1].record(stream)
+        torch.cuda.synchronize()
+        t_dense = de[0].elapsed_time(de[1]) / dense_steps
+        print(f"[bench] dense {t_dense:.3f} ms", file=sys.stderr, flush=True)
+    res = {
+        "ms_total": ms_total, "t_est": t_est, "t_sel": t_sel, "t_attn": t_attn, "t_dense": t_dense,
+        "sparsity": 1.0 - total_blocks / causal_blocks, "total_blocks": total_blocks,
+        "f_dense": f_dense, "f_attn": f_attn, "achieved": achieved, "peak": peak,
+        "head_count_min": int(counts.min()), "head_count_median": float(np.median(counts)),
+        "head_count_max": int(counts.max()),
+        "dense_mfma_frac": (4.0 * b * b * d * causal_blocks / (t_dense * 1e-3) / 1e12 / peak)
+        if t_dense else None,
+    }
+    return res, host, inputs
+
+
+def summary_line(wl, r, steps):
+    return {
+        "workload": wl.name, "seq_len": wl.seq_len, "gamma": wl.gamma,
+        "head_deviation": wl.structure.noise, "num_proxy_groups": wl.num_proxy_groups,
+        "min_budget_tokens": wl.min_budget_tokens, "steps": steps,
+        "ms_per_step": round(r["ms_total"], 4), "t_estimate_ms": round(r["t_est"], 4),
+        "t_select_ms": round(r["t_sel"], 4), "t_attention_ms": round(r["t_attn"], 4),
+        "t_dense_ms": round(r["t_dense"], 4) if r["t_dense"] else None,
+        "speedup_vs_dense": round(r["t_dense"] / r["ms_total"], 3) if r["t_dense"] else None,
+        "dense_equiv_tflops": round(r["f_dense"] / (r["ms_total"] * 1e-3) / 1e12, 2),
+        "estimation_overhead_pct": round(100.0 * (r["t_est"] + r["t_sel"]) / r["ms_total"], 2),
+        "sparsity": round(r["sparsity"], 4), "computed_blocks": r["total_blocks"],
+        "attn_mfma_frac": round(r["achieved"] / r["peak"], 4),
+        "dense_mfma_frac": round(r["dense_mfma_frac"], 4) if r["dense_mfma_frac"] else None,
+        "head_count_min_median_max": [r["head_count_min"], r["head_count_median"],
+                                      r["head_count_max"]],
+    }
+
+
+SWEEPS = {
+    # the 128K layer over thresholds and head similarity
+    "gamma_sigma_128k": [("llama3_8b_n131072", dict(gamma=g, noise=s))
+                         for s in (0.1, 0.3, 0.6) for g in (0.9, 0.95, 0.99)],
+    # the 32K layer
+    "llama_32k": [("llama3_8b_n32768", {})],
+    # heterogeneous Qwen-shaped layer over proxy groups and minimum budgets
+    "qwen_64k": [("qwen25_7b_n65536", dict(num_proxy_groups=g, min_budget_tokens=mb))
+                 for g in (1, 2, 4, 7) for mb in (0, 2048)],
+    # one layer of the 256K 32-layer stack (layer 0)
+    "llama_256k_layer": [("llama3_8b_n262144", {})],
+}
+
+
+def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
+    from paper_2509_24745_amd.synth import WORKLOADS
+    cache = {}
+    dense_cache = {}
+    for wname, kw in SWEEPS[name]:
+        wl = WORKLOADS[wname].replace(**kw) if kw else WORKLOADS[wname]
+        # inputs depend on the generator settings only (not on gamma, G, min budget)
+        key = (wname, wl.structure, wl.seed)
+        dkey = (wname,)
+        res, host, inputs = measure(wl, steps, warmup, dense_steps,
+                                    with_dense=dkey not in dense_cache, inputs=cache.get(key))
+        cache = {key: inputs}
+        if res["t_dense"] is None:
+            res["t_dense"] = dense_cache[dkey]["t_dense"]
+            res["dense_mfma_frac"] = dense_cache[dkey]["dense_mfma_frac"]
+        else:
+            dense_cache[dkey] = res
+        print(json.dumps(summary_line(wl, res, steps)), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -128,8 +273,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n}))
         return
-    from paper_2509_24745_amd import proxyattn as pa
-    from paper_2509_24745_amd.synth import WORKLOADS, generate
+    from paper_2509_24745_amd.synth import WORKLOADS
+    if args.sweep:
+        run_sweep(args.sweep, args.steps, args.warmup, args.dense_steps)
+        return
 
     wl = WORKLOADS[args.workload]
     kw = {}
@@ -142,74 +289,12 @@ def main():
     if args.min_budget is not None:
         kw["min_budget_tokens"] = args.min_budget
     wl = wl.replace(**kw) if kw else wl
-    print(f"[bench] generating {wl.name} N={wl.seq_len} gamma={wl.gamma} "
-          f"sigma={wl.structure.noise}", file=sys.stderr, flush=True)
-    t = time.time()
-    g = generate(wl)
-    print(f"[bench] generated in {time.time() - t:.1f}s", file=sys.stderr, flush=True)
-    prob = pa.Problem(seq_len=wl.seq_len, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
-                      head_dim=wl.head_dim, block_size=wl.block_size,
-                      num_proxy_groups=wl.num_proxy_groups, stride=wl.stride, dtype=wl.dtype)
-    dt = prob.torch_dtype
-    q = torch.from_numpy(g["q"]).to(dt).cuda()
-    k = torch.from_numpy(g["k"]).to(dt).cuda()
-    v = torch.from_numpy(g["v"]).to(dt).cuda()
-    bufs = pa.Buffers(prob)
-    stream = torch.cuda.current_stream()
-
-    def step(ev=None):
-        if ev: ev[0].record(stream)
-        pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, stream)
-        if ev: ev[1].record(stream)
-        pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma, wl.min_budget_tokens,
-                                   bufs.head_count, bufs.block_count, bufs.block_index, stream)
-        if ev: ev[2].record(stream)
-        pa.proxyattn_block_sparse_prefill(prob, q, k, v, bufs.block_count, bufs.block_index,
-                                          bufs.out, bufs.lse, bufs.workspace, stream)
-        if ev: ev[3].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    start.record(stream)
-    for i in range(args.steps):
-        step(evs[i])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_total = start.elapsed_time(stop) / args.steps
-    t_est = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    t_sel = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    print(f"[bench] {args.steps} steps: {ms_total:.3f} ms/step (est {t_est:.3f}, sel {t_sel:.3f}, "
-          f"attn {t_attn:.3f}); host wall {wall:.2f}s", file=sys.stderr, flush=True)
-
-    mq, hq, d, b, n = prob.num_blocks, prob.num_q_heads, prob.head_dim, prob.block_size, prob.seq_len
-    total_blocks = int(bufs.block_count.sum().item())
-    causal_blocks = hq * mq * (mq + 1) // 2
-    sparsity = 1.0 - total_blocks / causal_blocks
-    f_dense = 4.0 * hq * d * n * (n + 1) / 2          # dense-equivalent causal flops
-    f_attn = 4.0 * b * b * d * total_blocks            # flops the sparse kernel computes
-    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
-    achieved = f_attn / (t_attn * 1e-3) / 1e12
-
-    t_dense = None
-    if not args.no_dense:
-        de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        dense_out = torch.empty_like(bufs.out)
-        pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
-        torch.cuda.synchronize()
-        de[0].record(stream)
-        for _ in range(args.dense_steps):
-            pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
-        de[1].record(stream)
-        torch.cuda.synchronize()
-        t_dense = de[0].elapsed_time(de[1]) / args.dense_steps
-        print(f"[bench] dense {t_dense:.3f} ms", file=sys.stderr, flush=True)
+    r, g, _ = measure(wl, args.steps, args.warmup, args.dense_steps, with_dense=not args.no_dense)
+    ms_total, t_est, t_sel, t_attn, t_dense = r["ms_total"], r["t_est"], r["t_sel"], r["t_attn"], r["t_dense"]
+    n, hq, d, b = wl.seq_len, wl.num_q_heads, wl.head_dim, wl.block_size
+    mq = wl.num_blocks
+    sparsity, total_blocks, f_dense, achieved, peak = (r["sparsity"], r["total_blocks"], r["f_dense"],
+                                                       r["achieved"], r["peak"])
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -230,8 +315,8 @@ def main():
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "seq_len": n, "num_q_heads": hq,
-                   "num_kv_heads": prob.num_kv_heads, "head_dim": d, "block_size": b,
-                   "num_proxy_groups": prob.num_proxy_groups, "stride": prob.stride,
+                   "num_kv_heads": wl.num_kv_heads, "head_dim": d, "block_size": b,
+                   "num_proxy_groups": wl.num_proxy_groups, "stride": wl.stride,
                    "gamma": wl.gamma, "head_deviation": wl.structure.noise,
                    "min_budget_tokens": wl.min_budget_tokens, "parallelism": "single GPU"},
         "t_estimate_ms": round(t_est, 4),
@@ -244,8 +329,7 @@ def main():
         "speedup_vs_dense": round(t_dense / ms_total, 3) if t_dense else None,
         "estimation_overhead_pct_of_dense": round(100.0 * (t_est + t_sel) / t_dense, 2)
         if t_dense else None,
-        "dense_mfma_frac": round(4.0 * b * b * d * hq * mq * (mq + 1) / 2 / (t_dense * 1e-3)
-                                 / 1e12 / peak, 4) if t_dense else None,
+        "dense_mfma_frac": round(r["dense_mfma_frac"], 4) if t_dense else None,
         "computed_blocks": total_blocks,
         "roofline": {"kernel": "attn_kernel (block-sparse prefill call)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
