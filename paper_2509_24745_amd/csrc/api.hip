@@ -116,6 +116,7 @@ WsLayout ws_layout(const Shape& sh) {
     L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.nchunks * sh.b * 2 * 4);
     L.kvb = off;  off = align_up(off + (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz);
+    L.queue = off; off = align_up(off + (size_t)kNumXcd * kQueueStride * 4);
     L.total = off;
     return L;
 }
@@ -243,8 +244,10 @@ static int prefill_common(const proxyattn_problem* p, const void* q, const void*
     PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    PA_LAUNCH(launch_kv_block(sh, k, v, ws + L.kvb, st), "kv_block");
-    PA_LAUNCH(launch_attention(sh, dense, q, ws + L.kvb, block_count, block_index, out, lse, st),
+    int* queue = (int*)(ws + L.queue);
+    PA_LAUNCH(launch_kv_block(sh, k, v, ws + L.kvb, queue, st), "kv_block");
+    PA_LAUNCH(launch_attention(sh, dense, q, ws + L.kvb, block_count, block_index, out, lse, queue,
+                               st),
               "attention");
     return PROXYATTN_OK;
 }

@@ -30,6 +30,10 @@
 //     instruction with the softmax of step j (VALU) in one basic block, then
 //     PV of step j runs; the row max of step j+1 closes the step, so the
 //     rare rescale branch stays out of that block.
+#include <algorithm>
+#include <mutex>
+#include <vector>
+
 #include "common.h"
 #include "internal.h"
 
@@ -40,14 +44,19 @@ __device__ __forceinline__ int swap_bits23(int x) {
 }
 
 // ---------------------------------------------------------------------------
-// K, V -> kvb.  grid (Mq, Hkv), 256 threads.  Rows >= N are zero.
+// K, V -> kvb.  grid (Mq, Hkv), 256 threads.  Rows >= N are zero.  Also
+// zeroes the attention work-queue counters.
 // ---------------------------------------------------------------------------
 constexpr int kSubKeys = 64;  // keys per attention sub-block
 
 template <typename T, int D, int B>
 __global__ __launch_bounds__(256) void kv_block_kernel(Shape sh, const T* __restrict__ k,
                                                        const T* __restrict__ v,
-                                                       T* __restrict__ kvb) {
+                                                       T* __restrict__ kvb,
+                                                       int* __restrict__ queue) {
+    static_assert(kNumXcd * kQueueStride <= 256, "one thread per queue word");
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < kNumXcd * kQueueStride)
+        queue[threadIdx.x] = 0;
     constexpr int V = Vec16<T>::n;
     constexpr int LDR = D + V;
     constexpr int KT = kSubKeys < B ? kSubKeys : B;
@@ -88,7 +97,8 @@ __global__ __launch_bounds__(256) void kv_block_kernel(Shape sh, const T* __rest
 }
 
 // ---------------------------------------------------------------------------
-// attention.  grid attn_grid(sh), 2B threads (B/32 waves), 2 workgroups per CU.
+// attention.  Persistent grid (one workgroup per resident slot), 2B threads (B/32
+// waves), 2 workgroups per CU.
 // ---------------------------------------------------------------------------
 template <typename T> __device__ __forceinline__ T cvt_p(float p);
 template <> __device__ __forceinline__ bf16 cvt_p<bf16>(float p) { return (bf16)p; }
@@ -114,8 +124,10 @@ struct AttnCfg {
     static constexpr int VPT = SUB / V / NTH;          // 16-byte vectors per thread per sub-block
 };
 
-// Work item of workgroup `b`.  Workgroups are dealt to the XCDs round-robin:
-// XCD x = b % 8 sees its workgroups in slot order b / 8.
+// Work item number `b` (b % 8 = queue, b / 8 = position in that queue).  The
+// queues are drained by the persistent workgroups of one XCD each (workgroup
+// w serves queue w % 8: workgroups are dealt to the XCDs round-robin), so
+// queue x is XCD x's work in the order it is taken.
 // Order 0: longest block rows first, heads fastest.
 // Order 1 (row chunks): chunks of R consecutive block rows (longest first)
 //   x all query heads, KV heads outermost inside a chunk; chunk c runs on
@@ -161,9 +173,10 @@ __device__ __forceinline__ bool attn_item(const Shape& sh, int b, int* m_out, in
     return true;
 }
 
-static int attn_grid(const Shape& sh) {
+// Number of work-item numbers (a multiple of kNumXcd; some are padding).
+__host__ __device__ __forceinline__ int attn_items(const Shape& sh) {
     const int R = sh.attn_chunk_rows;
-    if (sh.attn_order == 0 || R <= 0) return sh.hq * sh.mq;
+    if (sh.attn_order == 0 || R <= 0) return kNumXcd * ((sh.hq * sh.mq + kNumXcd - 1) / kNumXcd);
     if (sh.attn_order == 1) {
         const int chunks = (sh.mq + R - 1) / R;
         return kNumXcd * ((chunks + kNumXcd - 1) / kNumXcd) * sh.hq * R;
@@ -173,24 +186,24 @@ static int attn_grid(const Shape& sh) {
 }
 
 // Direct global -> LDS copy of one kvb sub-block (K rows, then V^T rows)
-// into the padded LDS layout.  One global_load_lds_dwordx4 moves 64
+// into the padded LDS layout.  One buffer_load_dwordx4 ... lds moves 64
 // consecutive 16-byte LDS slots (slot = lane); the padded layout has one
 // spare slot per row, which loads a harmless duplicate of the row's first
-// chunk.  Instructions are dealt to the waves round-robin; each lane's byte
-// offsets inside a sub-block are loop invariant and computed once.
-template <typename T, int D, int B>
+// chunk.  The buffer descriptor spans exactly the sub-block (built in SGPRs
+// per copy), so each lane needs one 32-bit offset per instruction, computed
+// once, and the hardware range check keeps every read inside the sub-block.
+// Instructions are dealt to the waves round-robin.
+template <typename T, int D, int KT, int NW>
 struct SubTileDma {
-    typedef AttnCfg<T, D, B> C;
-    static constexpr int V = C::V;
-    static constexpr int NW = C::NTH / 64;
+    static constexpr int V = Vec16<T>::n;
     static constexpr int KSR = D / V + 1;              // slots per padded K row
-    static constexpr int VSR = C::KT / V + 1;          // slots per padded V^T row
-    static constexpr int K_INS = C::KT * KSR / 64;     // wave instructions, K part
+    static constexpr int VSR = KT / V + 1;             // slots per padded V^T row
+    static constexpr int K_INS = KT * KSR / 64;        // wave instructions, K part
     static constexpr int V_INS = D * VSR / 64;         // wave instructions, V^T part
     static constexpr int KJ = (K_INS + NW - 1) / NW;   // per wave (upper bound)
     static constexpr int VJ = (V_INS + NW - 1) / NW;
-    static_assert(C::KT * KSR % 64 == 0 && D * VSR % 64 == 0, "whole wave instructions");
-    static_assert(C::KPAD == KSR * V && C::VPAD == VSR * V, "padded pitches");
+    static constexpr int SUB_BYTES = 2 * KT * D * (int)sizeof(T);
+    static_assert(KT * KSR % 64 == 0 && D * VSR % 64 == 0, "whole wave instructions");
 
     uint32_t koff[KJ], voff[VJ];   // byte offsets inside a sub-block
     int w;
@@ -206,27 +219,33 @@ struct SubTileDma {
         for (int j = 0; j < VJ; ++j) {
             const int slot = (w + j * NW) * 64 + lane;
             const int row = slot / VSR, ch = slot % VSR;
-            voff[j] = (uint32_t)((C::KT * D + row * C::KT + (ch == VSR - 1 ? 0 : ch * V)) * sizeof(T));
+            voff[j] = (uint32_t)((KT * D + row * KT + (ch == VSR - 1 ? 0 : ch * V)) * sizeof(T));
         }
     }
-    __device__ __forceinline__ void issue_k(const T* src, T* k_lds) const {
-        const char* base = reinterpret_cast<const char*>(src);
+    static __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const T* sub) {
+        // raw buffer, 32-bit dword format (CDNA descriptor word 3)
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(sub), 0, SUB_BYTES, 0x00020000);
+    }
+    __device__ __forceinline__ void issue_k(const T* sub, T* k_lds) const {
+        const __amdgpu_buffer_rsrc_t r = rsrc(sub);
 #pragma unroll
         for (int j = 0; j < KJ; ++j) {
             const int ins = w + j * NW;
             if (KJ * NW == K_INS || ins < K_INS)
-                __builtin_amdgcn_global_load_lds((const void*)(base + koff[j]),
-                                                 (void*)(k_lds + ins * 64 * V), 16, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    r, (__attribute__((address_space(3))) void*)(k_lds + ins * 64 * V), 16, koff[j],
+                    0, 0, 0);
         }
     }
-    __device__ __forceinline__ void issue_v(const T* src, T* v_lds) const {
-        const char* base = reinterpret_cast<const char*>(src);
+    __device__ __forceinline__ void issue_v(const T* sub, T* v_lds) const {
+        const __amdgpu_buffer_rsrc_t r = rsrc(sub);
 #pragma unroll
         for (int j = 0; j < VJ; ++j) {
             const int ins = w + j * NW;
             if (VJ * NW == V_INS || ins < V_INS)
-                __builtin_amdgcn_global_load_lds((const void*)(base + voff[j]),
-                                                 (void*)(v_lds + ins * 64 * V), 16, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    r, (__attribute__((address_space(3))) void*)(v_lds + ins * 64 * V), 16, voff[j],
+                    0, 0, 0);
         }
     }
 };
@@ -254,8 +273,7 @@ __device__ __forceinline__ float tile_max(const f32x16* s) {
     for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; r += 2) c[(r >> 1) & 3] = fmaxf(c[(r >> 1) & 3], fmaxf(s[kt][r], s[kt][r + 1]));
-    const float mx = fmaxf(fmaxf(c[0], c[1]), fmaxf(c[2], c[3]));
-    return fmaxf(mx, swap_halves(mx));
+    return halves_max(fmaxf(fmaxf(c[0], c[1]), fmaxf(c[2], c[3])));
 }
 
 // Sum of the probabilities a lane feeds to the PV product.  bf16: two per
@@ -292,26 +310,29 @@ __device__ __forceinline__ float prob_sum<float, 2>(const f32x8 (*pf)[2]) {
     return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
+// One work item: query block m of query head i.  Every wave of the
+// workgroup calls it with the same (m, i); it starts and ends with no copy
+// in flight, and the caller's barrier separates it from the previous item's
+// LDS reads.
 template <typename T, int D, int B, bool DENSE>
-__global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __restrict__ q,
-                                                        const T* __restrict__ kvb,
-                                                        const int* __restrict__ block_count,
-                                                        const int* __restrict__ block_index,
-                                                        T* __restrict__ out,
-                                                        float* __restrict__ lse) {
+__device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ q,
+                                         const T* __restrict__ kvb,
+                                         const int* __restrict__ block_count,
+                                         const int* __restrict__ block_index,
+                                         T* __restrict__ out, float* __restrict__ lse,
+                                         const int m, const int i,
+                                         T (&ks_buf)[2][AttnCfg<T, D, B>::K_ELEMS],
+                                         T (&vs_buf)[2][AttnCfg<T, D, B>::V_ELEMS]) {
     typedef AttnCfg<T, D, B> C;
     typedef typename FragOf<T>::type Frag;
-    typedef SubTileDma<T, D, B> Dma;
+    typedef SubTileDma<T, D, C::KT, C::NTH / 64> Dma;
+    static_assert(C::KPAD == Dma::KSR * C::V && C::VPAD == Dma::VSR * C::V, "padded pitches");
     constexpr int NT = C::NT;
     constexpr int DT = D / 32;   // output tiles along d
     constexpr int KS = D / 16;   // k steps of Q K^T
     static_assert(NT == 2, "64-key sub-tiles");
-    __shared__ __attribute__((aligned(16))) T ks_buf[2][C::K_ELEMS];
-    __shared__ __attribute__((aligned(16))) T vs_buf[2][C::V_ELEMS];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
-    int m, i;
-    if (!attn_item(sh, blockIdx.x, &m, &i)) return;
     const int kvh = i / sh.rep;
     const int n_tok = sh.n;
     // counts and indices are clamped to the causal range, so malformed caller
@@ -325,7 +346,11 @@ __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __res
     if (cnt <= 0) {
         if (qvalid) {
             T* orow = out + (int64_t)qtok * sh.o_tok + (int64_t)i * sh.o_head;
-            for (int e = h; e < D; e += 2) orow[e] = from_f32_rne<T>(0.f);
+            // lane half h zeroes elements [h D/2, (h+1) D/2); a rolled loop,
+            // so that no per-lane address stays live across work items
+            u32x4* o4 = reinterpret_cast<u32x4*>(orow + h * (D / 2));
+#pragma unroll 1
+            for (int e = 0; e < D / 2 / Vec16<T>::n; ++e) o4[e] = zero_u32x4();
             if (lse && h == 0) lse[(int64_t)i * n_tok + qtok] = kNegInf;
         }
         return;
@@ -466,7 +491,7 @@ __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __res
         if (st + 1 < steps) step(s_alt, s_cur, st + 1);
     }
 
-    const float l_tot = l_run + swap_halves(l_run);
+    const float l_tot = halves_sum(l_run);
     const float inv = 1.f / l_tot;
     if (qvalid) {
         T* orow = out + (int64_t)qtok * sh.o_tok + (int64_t)i * sh.o_head;
@@ -489,51 +514,122 @@ __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __res
     }
 }
 
+// Persistent kernel: one resident workgroup per slot (2B threads, B/32
+// waves); workgroup w takes the next item of queue w % 8 until the queue is
+// empty.  Taking work dynamically keeps every slot busy whatever the mix of
+// list lengths: the hardware dispatcher hands workgroups to the shader
+// engines of an XCD in a fixed rotation, so a grid of one workgroup per item
+// lets the engines that receive the long items hold back all the others.
+template <typename T, int D, int B, bool DENSE>
+__global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __restrict__ q,
+                                                        const T* __restrict__ kvb,
+                                                        const int* __restrict__ block_count,
+                                                        const int* __restrict__ block_index,
+                                                        T* __restrict__ out,
+                                                        float* __restrict__ lse,
+                                                        int* __restrict__ queue) {
+    typedef AttnCfg<T, D, B> C;
+    __shared__ __attribute__((aligned(16))) T ks_buf[2][C::K_ELEMS];
+    __shared__ __attribute__((aligned(16))) T vs_buf[2][C::V_ELEMS];
+    __shared__ int next_item;
+    const int x = blockIdx.x % kNumXcd;
+    const int per_queue = attn_items(sh) / kNumXcd;
+    int* counter = queue + x * kQueueStride;
+    for (;;) {
+        // the barrier also keeps the previous item's LDS reads ahead of the
+        // next item's copies
+        if (threadIdx.x == 0) next_item = atomicAdd(counter, 1);
+        __syncthreads();
+        const int pos = next_item;
+        __syncthreads();
+        if (pos >= per_queue) break;
+        int m, i;
+        if (!attn_item(sh, x + kNumXcd * pos, &m, &i)) continue;
+        attn_one<T, D, B, DENSE>(sh, q, kvb, block_count, block_index, out, lse, m, i, ks_buf,
+                                 vs_buf);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 template <typename T, int D, int B>
-static hipError_t kvb_t(const Shape& sh, const void* k, const void* v, void* kvb, hipStream_t st) {
+static hipError_t kvb_t(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,
+                        hipStream_t st) {
     hipLaunchKernelGGL((kv_block_kernel<T, D, B>), dim3(sh.mq, sh.hkv), dim3(256), 0, st, sh,
-                       (const T*)k, (const T*)v, (T*)kvb);
+                       (const T*)k, (const T*)v, (T*)kvb, queue);
     return hipGetLastError();
 }
 
-hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb,
+hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,
                            hipStream_t st) {
     if (sh.dtype == 0) {
-        if (sh.d == 64) return sh.b == 64 ? kvb_t<bf16, 64, 64>(sh, k, v, kvb, st) : kvb_t<bf16, 64, 128>(sh, k, v, kvb, st);
-        return sh.b == 64 ? kvb_t<bf16, 128, 64>(sh, k, v, kvb, st) : kvb_t<bf16, 128, 128>(sh, k, v, kvb, st);
+        if (sh.d == 64) return sh.b == 64 ? kvb_t<bf16, 64, 64>(sh, k, v, kvb, queue, st) : kvb_t<bf16, 64, 128>(sh, k, v, kvb, queue, st);
+        return sh.b == 64 ? kvb_t<bf16, 128, 64>(sh, k, v, kvb, queue, st) : kvb_t<bf16, 128, 128>(sh, k, v, kvb, queue, st);
     }
-    if (sh.d == 64) return sh.b == 64 ? kvb_t<float, 64, 64>(sh, k, v, kvb, st) : kvb_t<float, 64, 128>(sh, k, v, kvb, st);
-    return sh.b == 64 ? kvb_t<float, 128, 64>(sh, k, v, kvb, st) : kvb_t<float, 128, 128>(sh, k, v, kvb, st);
+    if (sh.d == 64) return sh.b == 64 ? kvb_t<float, 64, 64>(sh, k, v, kvb, queue, st) : kvb_t<float, 64, 128>(sh, k, v, kvb, queue, st);
+    return sh.b == 64 ? kvb_t<float, 128, 64>(sh, k, v, kvb, queue, st) : kvb_t<float, 128, 128>(sh, k, v, kvb, queue, st);
+}
+
+// Workgroups of `fn` (with `threads` threads) resident on the current device
+// at once, rounded down to a multiple of kNumXcd (at least kNumXcd, so that
+// every queue has a workgroup).  Cached per (device, kernel).
+static int resident_grid(const void* fn, int threads, int* grid) {
+    struct Entry { int dev; const void* fn; int grid; };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return (int)e;
+    {
+        std::lock_guard<std::mutex> lk(mu);
+        for (const Entry& c : cache)
+            if (c.dev == dev && c.fn == fn) { *grid = c.grid; return 0; }
+    }
+    int cus = 0, per_cu = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return (int)e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, 0);
+    if (e != hipSuccess) return (int)e;
+    const int g = per_cu * cus / kNumXcd * kNumXcd;
+    *grid = g < kNumXcd ? kNumXcd : g;
+    std::lock_guard<std::mutex> lk(mu);
+    cache.push_back({dev, fn, *grid});
+    return 0;
 }
 
 template <typename T, int D, int B>
 static hipError_t attn_t(const Shape& sh, bool dense, const void* q, const void* kvb,
-                         const int* bc, const int* bi, void* out, float* lse, hipStream_t st) {
-    const dim3 grid((unsigned)attn_grid(sh));
+                         const int* bc, const int* bi, void* out, float* lse, int* queue,
+                         hipStream_t st) {
+    const void* fn = dense ? (const void*)attn_kernel<T, D, B, true>
+                           : (const void*)attn_kernel<T, D, B, false>;
+    int g = 0;
+    const int e = resident_grid(fn, 2 * B, &g);
+    if (e) return (hipError_t)e;
+    const dim3 grid((unsigned)std::min(g, attn_items(sh)));
     if (dense)
         hipLaunchKernelGGL((attn_kernel<T, D, B, true>), grid, dim3(2 * B), 0, st, sh,
-                           (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse);
+                           (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse, queue);
     else
         hipLaunchKernelGGL((attn_kernel<T, D, B, false>), grid, dim3(2 * B), 0, st, sh,
-                           (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse);
+                           (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse, queue);
     return hipGetLastError();
 }
 
 hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* kvb,
-                            const int* bc, const int* bi, void* out, float* lse, hipStream_t st) {
+                            const int* bc, const int* bi, void* out, float* lse, int* queue,
+                            hipStream_t st) {
     if (sh.dtype == 0) {
-        if (sh.d == 64) return sh.b == 64 ? attn_t<bf16, 64, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
-                                          : attn_t<bf16, 64, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
-        return sh.b == 64 ? attn_t<bf16, 128, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
-                          : attn_t<bf16, 128, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
+        if (sh.d == 64) return sh.b == 64 ? attn_t<bf16, 64, 64>(sh, dense, q, kvb, bc, bi, out, lse, queue, st)
+                                          : attn_t<bf16, 64, 128>(sh, dense, q, kvb, bc, bi, out, lse, queue, st);
+        return sh.b == 64 ? attn_t<bf16, 128, 64>(sh, dense, q, kvb, bc, bi, out, lse, queue, st)
+                          : attn_t<bf16, 128, 128>(sh, dense, q, kvb, bc, bi, out, lse, queue, st);
     }
-    if (sh.d == 64) return sh.b == 64 ? attn_t<float, 64, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
-                                      : attn_t<float, 64, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
-    return sh.b == 64 ? attn_t<float, 128, 64>(sh, dense, q, kvb, bc, bi, out, lse, st)
-                      : attn_t<float, 128, 128>(sh, dense, q, kvb, bc, bi, out, lse, st);
+    if (sh.d == 64) return sh.b == 64 ? attn_t<float, 64, 64>(sh, dense, q, kvb, bc, bi, out, lse, queue, st)
+                                      : attn_t<float, 64, 128>(sh, dense, q, kvb, bc, bi, out, lse, queue, st);
+    return sh.b == 64 ? attn_t<float, 128, 64>(sh, dense, q, kvb, bc, bi, out, lse, queue, st)
+                      : attn_t<float, 128, 128>(sh, dense, q, kvb, bc, bi, out, lse, queue, st);
 }
 
 }  // namespace pa

@@ -112,8 +112,23 @@ template <> __device__ __forceinline__ bf16 from_f32_rne<bf16>(float x) { return
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-// Value held by lane (l ^ 32): exchange between the two wave halves.
-__device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }
+// Exchanges between the two wave halves without LDS: v_permlane32_swap of x
+// with itself gives, in every lane l, r[0] = x[l % 32] and r[1] = x[l % 32 + 32].
+__device__ __forceinline__ float swap_halves(float x) {   // x of lane l ^ 32
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return __uint_as_float((__lane_id() & 32) ? r[0] : r[1]);
+}
+__device__ __forceinline__ float halves_max(float x) {    // max of lanes l and l ^ 32
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {    // x[l % 32] + x[l % 32 + 32]
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll

@@ -37,6 +37,10 @@ struct Shape {
 // Number of XCDs workgroups are dealt to round-robin on MI355X.
 constexpr int kNumXcd = 8;
 
+// The attention kernel is persistent: its workgroups pull work items from
+// kNumXcd queues (one int32 counter per queue, each on its own 128-byte line).
+constexpr int kQueueStride = 32;
+
 // Keys per chunk of the last-block mass kernels (a multiple of every block size).
 constexpr int kMassChunk = 2048;
 
@@ -48,6 +52,7 @@ struct WsLayout {
                      // [G][Mq(Mq+1)/2][b'] fp32 (lower-triangular block pairs)
     size_t part;     // last-block partial (max, sum) [Hq][nchunks][b][2] fp32
     size_t kvb;      // re-blocked K and V^T [Hkv][Mq][2 b d] (problem dtype)
+    size_t queue;    // attention work-queue counters [kNumXcd][kQueueStride] int32
     size_t total;
 };
 
@@ -65,10 +70,12 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
                          int* block_count, int* block_index, hipStream_t st);
-hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb,
+// launch_kv_block also resets the attention work queues; launch_attention
+// must follow it on the same stream.
+hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,
                            hipStream_t st);
 hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* kvb,
                             const int* block_count, const int* block_index, void* out, float* lse,
-                            hipStream_t st);
+                            int* queue, hipStream_t st);
 
 }  // namespace pa
