@@ -80,26 +80,30 @@ __device__ __forceinline__ f32x16 st_tile(const T* lds_tile, const typename Frag
 
 // ---------------------------------------------------------------------------
 // a2: proxy row normaliser and per-(row, key block) max
-// grid (ceil(N'/128), G), 256 threads; wave w owns strided rows R0+32w..+31.
+// grid (ceil(N'/128), G), 256 threads; workgroup x takes the strided rows
+// R0 = (gridDim.x - 1 - x) * 128 .. +127 (longest rows first), wave w rows
+// R0+32w..+31.  Only the wave's diagonal key tile needs the causal mask.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int BP>
-__global__ __launch_bounds__(256) void est_rowmax_kernel(Shape sh, const T* __restrict__ qg,
-                                                         const T* __restrict__ kg,
-                                                         float* __restrict__ rbm,
-                                                         float* __restrict__ lse2) {
+__global__ __launch_bounds__(256, 2) void est_rowmax_kernel(Shape sh, const T* __restrict__ qg,
+                                                            const T* __restrict__ kg,
+                                                            float* __restrict__ rbm,
+                                                            float* __restrict__ lse2) {
     typedef typename FragOf<T>::type Frag;
     constexpr int KS = D / 16;
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, 256>::LDT];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
     const int g = blockIdx.y;
     const int np = sh.np;
-    const int R0 = blockIdx.x * 128;
+    const int R0 = (gridDim.x - 1 - blockIdx.x) * 128;
     const T* qbase = qg + (int64_t)g * np * D;
     const T* kbase = kg + (int64_t)g * np * D;
     const int row = R0 + 32 * w + lc;
     const bool wave_on = R0 + 32 * w < np;
-    const int wave_last_tile = wave_on ? min(R0 + 32 * w + 31, np - 1) / 32 : -1;
+    const int diag_tile = (R0 + 32 * w) / 32;   // the wave's rows all lie in this key tile
+    const int wave_last_tile = wave_on ? diag_tile : -1;
     const int last_tile = min(R0 + 127, np - 1) / 32;
+    const float scale2 = sh.scale2;
 
     Frag qf[KS];
     {
@@ -110,6 +114,7 @@ __global__ __launch_bounds__(256) void est_rowmax_kernel(Shape sh, const T* __re
     const int64_t tri_total = (int64_t)sh.mq * (sh.mq + 1) / 2;
     float* rbm_g = rbm + (int64_t)g * tri_total * BP;
 
+    // running max m (scaled, log2 units) and sum l of exp2(c' s - m)
     float m = kNegInf, l = 0.f, bm = kNegInf;
     KeyTile<T, D, 256> kt_ld;
     kt_ld.load(kbase, D, 0, np, tid);
@@ -118,30 +123,32 @@ __global__ __launch_bounds__(256) void est_rowmax_kernel(Shape sh, const T* __re
     for (int kt = 0; kt <= last_tile; ++kt) {
         if (kt < last_tile) kt_ld.load(kbase, D, (kt + 1) * 32, np, tid);
         if (kt <= wave_last_tile) {
-            const f32x16 acc = st_tile<T, D>(tiles[kt & 1], qf, lc, h);
-            float x[16];
-            float tm = kNegInf;
+            f32x16 acc = st_tile<T, D>(tiles[kt & 1], qf, lc, h);
+            if (kt == diag_tile) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int u = kt * 32 + c_row(r, h);
-                x[r] = (u <= row) ? acc[r] * sh.scale2 : kNegInf;
-                tm = fmaxf(tm, x[r]);
+                for (int r = 0; r < 16; ++r)
+                    acc[r] = (kt * 32 + c_row(r, h) <= row) ? acc[r] : kNegInf;
             }
+            // raw maxima (the scale is positive, so it commutes with max)
+            float c4[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                c4[j] = fmaxf(fmaxf(acc[4 * j], acc[4 * j + 1]), fmaxf(acc[4 * j + 2], acc[4 * j + 3]));
+            const float tm = fmaxf(fmaxf(c4[0], c4[1]), fmaxf(c4[2], c4[3])) * scale2;
+            // a lane half can have all of its keys masked so far (mn = -inf):
+            // it then adds exp2(-inf) = 0 and keeps l = 0
             const float mn = fmaxf(m, tm);
-            if (mn != kNegInf) {
-                float sum = 0.f;
+            const float neg = (mn == kNegInf) ? 0.f : -mn;
+            const float alpha = (m == kNegInf) ? 0.f : fast_exp2(m - mn);
+            float sp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int r = 0; r < 16; ++r) sum += exp2f(x[r] - mn);
-                l = l * exp2f(m - mn) + sum;
-                m = mn;
-            }
+            for (int r = 0; r < 16; ++r) sp[r & 3] += fast_exp2(fmaf(acc[r], scale2, neg));
+            l = fmaf(l, alpha, (sp[0] + sp[1]) + (sp[2] + sp[3]));
+            m = mn;
             if constexpr (BP == 16) {
                 // one 32-key tile holds two key blocks: slots r < 8 and r >= 8
-                float s0 = kNegInf, s1 = kNegInf;
-#pragma unroll
-                for (int r = 0; r < 8; ++r) { s0 = fmaxf(s0, x[r]); s1 = fmaxf(s1, x[r + 8]); }
-                s0 = fmaxf(s0, swap_halves(s0));
-                s1 = fmaxf(s1, swap_halves(s1));
+                const float s0 = halves_max(fmaxf(c4[0], c4[1]) * scale2);
+                const float s1 = halves_max(fmaxf(c4[2], c4[3]) * scale2);
                 if (h == 0 && row < np) {
                     const int mr = row / 16, j = row % 16, n0 = 2 * kt;
                     if (n0 <= mr) rbm_g[tri_index(mr, n0) * 16 + j] = s0;
@@ -149,7 +156,7 @@ __global__ __launch_bounds__(256) void est_rowmax_kernel(Shape sh, const T* __re
                 }
             } else {
                 constexpr int TPB = BP / 32;  // key tiles per block
-                const float sm = fmaxf(tm, swap_halves(tm));
+                const float sm = halves_max(tm);
                 bm = (kt % TPB == 0) ? sm : fmaxf(bm, sm);
                 if ((kt % TPB == TPB - 1 || kt == wave_last_tile) && h == 0 && row < np) {
                     const int mr = row / BP, j = row % BP, n = kt / TPB;
@@ -163,7 +170,9 @@ __global__ __launch_bounds__(256) void est_rowmax_kernel(Shape sh, const T* __re
     const float mo = swap_halves(m), lo = swap_halves(l);
     const float mm = fmaxf(m, mo);
     if (h == 0 && row < np) {
-        const float ll = l * exp2f(m - mm) + lo * exp2f(mo - mm);
+        // mm is finite (key 0 is visible to every row); a half with m = -inf has l = 0
+        const float ll = (m == kNegInf ? 0.f : l * fast_exp2(m - mm)) +
+                         (mo == kNegInf ? 0.f : lo * fast_exp2(mo - mm));
         lse2[(int64_t)g * np + row] = mm + log2f(ll);
     }
 }
@@ -208,7 +217,7 @@ __global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* 
 // a4: last-block mass.  grid (nchunks, Hq), B*2 threads (B/32 waves).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int B>
-__global__ __launch_bounds__(B * 2) void mass_partial_kernel(Shape sh, const T* __restrict__ q,
+__global__ __launch_bounds__(B * 2, 2) void mass_partial_kernel(Shape sh, const T* __restrict__ q,
                                                              const T* __restrict__ k,
                                                              float* __restrict__ part) {
     typedef typename FragOf<T>::type Frag;
@@ -220,6 +229,7 @@ __global__ __launch_bounds__(B * 2) void mass_partial_kernel(Shape sh, const T* 
     const int nrows = min(B, n), t0 = n - nrows;
     const int rl = 32 * w + lc, t = t0 + rl;
     const bool wave_on = 32 * w < nrows;
+    const int wave_first_t = t0 + 32 * w;
     const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
     const int key0 = c * kMassChunk, key1 = min(key0 + kMassChunk, n);
     const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
@@ -240,21 +250,25 @@ __global__ __launch_bounds__(B * 2) void mass_partial_kernel(Shape sh, const T* 
         const int buf = (kt - kt0) & 1;
         if (kt < kt1) ld.load(kbase, sh.kv_tok, (kt + 1) * 32, n, tid);
         if (wave_on && kt * 32 <= wave_last_t) {
-            const f32x16 acc = st_tile<T, D>(tiles[buf], qf, lc, h);
-            float x[16];
-            float tm = kNegInf;
+            f32x16 acc = st_tile<T, D>(tiles[buf], qf, lc, h);
+            // only tiles reaching past the wave's first row need the causal mask
+            if (kt * 32 + 31 > wave_first_t) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int u = kt * 32 + c_row(r, h);
-                x[r] = (u <= t) ? acc[r] * sh.scale2 : kNegInf;
-                tm = fmaxf(tm, x[r]);
+                for (int r = 0; r < 16; ++r)
+                    acc[r] = (kt * 32 + c_row(r, h) <= t) ? acc[r] : kNegInf;
             }
+            float c4[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                c4[j] = fmaxf(fmaxf(acc[4 * j], acc[4 * j + 1]), fmaxf(acc[4 * j + 2], acc[4 * j + 3]));
+            const float tm = fmaxf(fmaxf(c4[0], c4[1]), fmaxf(c4[2], c4[3])) * sh.scale2;
             const float mn = fmaxf(m, tm);
             if (mn != kNegInf) {
-                float sum = 0.f;
+                const float neg = -mn;
+                float sp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int r = 0; r < 16; ++r) sum += exp2f(x[r] - mn);
-                l = l * exp2f(m - mn) + sum;
+                for (int r = 0; r < 16; ++r) sp[r & 3] += fast_exp2(fmaf(acc[r], sh.scale2, neg));
+                l = fmaf(l, fast_exp2(m - mn), (sp[0] + sp[1]) + (sp[2] + sp[3]));
                 m = mn;
             }
         }
@@ -264,7 +278,7 @@ __global__ __launch_bounds__(B * 2) void mass_partial_kernel(Shape sh, const T* 
     const float mo = swap_halves(m), lo = swap_halves(l);
     const float mm = fmaxf(m, mo);
     if (h == 0 && rl < nrows) {
-        const float ll = (mm == kNegInf) ? 0.f : l * exp2f(m - mm) + lo * exp2f(mo - mm);
+        const float ll = (mm == kNegInf) ? 0.f : l * fast_exp2(m - mm) + lo * fast_exp2(mo - mm);
         float* pp = part + (((int64_t)i * sh.nchunks + c) * B + rl) * 2;
         pp[0] = mm;
         pp[1] = ll;
@@ -272,7 +286,7 @@ __global__ __launch_bounds__(B * 2) void mass_partial_kernel(Shape sh, const T* 
 }
 
 template <typename T, int D, int B>
-__global__ __launch_bounds__(B * 2) void mass_final_kernel(Shape sh, const T* __restrict__ q,
+__global__ __launch_bounds__(B * 2, 2) void mass_final_kernel(Shape sh, const T* __restrict__ q,
                                                            const T* __restrict__ k,
                                                            const float* __restrict__ part,
                                                            float* __restrict__ mass) {
@@ -287,7 +301,9 @@ __global__ __launch_bounds__(B * 2) void mass_final_kernel(Shape sh, const T* __
     const int nrows = min(B, n), t0 = n - nrows;
     const int rl = 32 * w + lc, t = t0 + rl;
     const bool wave_on = 32 * w < nrows;
+    const int wave_first_t = t0 + 32 * w;
     const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
+    const bool wave_full = 32 * w + 31 < nrows;
     const int key0 = c * kMassChunk, key1 = min(key0 + kMassChunk, n);
     const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
     const int blk0 = key0 / B, nblk = (key1 - key0 + B - 1) / B;
@@ -302,7 +318,7 @@ __global__ __launch_bounds__(B * 2) void mass_final_kernel(Shape sh, const T* __
         float s = 0.f;
         for (int cc = 0; cc < sh.nchunks; ++cc) {
             const float mc = pp[(int64_t)cc * B * 2], lcc = pp[(int64_t)cc * B * 2 + 1];
-            if (mc != kNegInf) s += lcc * exp2f(mc - mx);
+            if (mc != kNegInf) s += lcc * fast_exp2(mc - mx);
         }
         L2 = mx + log2f(s);
     }
@@ -322,12 +338,20 @@ __global__ __launch_bounds__(B * 2) void mass_final_kernel(Shape sh, const T* __
         if (kt < kt1) ld.load(kbase, sh.kv_tok, (kt + 1) * 32, n, tid);
         if (wave_on && kt * 32 <= wave_last_t) {
             const f32x16 acc = st_tile<T, D>(tiles[buf], qf, lc, h);
+            const float neg = -L2;
+            float sp[4] = {0.f, 0.f, 0.f, 0.f};
+            if (wave_full && kt * 32 + 31 <= wave_first_t) {
+                // every key of the tile is visible to every row of the wave
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int u = kt * 32 + c_row(r, h);
-                const float p = (u <= t && rl < nrows) ? exp2f(acc[r] * sh.scale2 - L2) : 0.f;
-                acc_blk += p;
+                for (int r = 0; r < 16; ++r) sp[r & 3] += fast_exp2(fmaf(acc[r], sh.scale2, neg));
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int u = kt * 32 + c_row(r, h);
+                    sp[r & 3] += (u <= t && rl < nrows) ? fast_exp2(fmaf(acc[r], sh.scale2, neg)) : 0.f;
+                }
             }
+            acc_blk += (sp[0] + sp[1]) + (sp[2] + sp[3]);
         }
         if (((kt + 1) * 32) % B == 0 || kt == kt1) {
             const float s = wave_sum(acc_blk);
