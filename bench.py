@@ -49,6 +49,14 @@ def parse():
     ap.add_argument("--sweep", choices=["gamma_sigma_128k", "llama_32k", "qwen_64k",
                                          "llama_256k_layer"], default=None,
                     help="print one JSON line per point of a workload sweep instead")
+    ap.add_argument("--stack", type=int, default=None, metavar="LAYERS",
+                    help="time a stack of LAYERS layers of --workload (layer l drawn with seed l; "
+                         "one JSON line per layer, then the totals)")
+    ap.add_argument("--stack-workers", type=int, default=4,
+                    help="processes generating stack layers ahead of the GPU")
+    ap.add_argument("--profile-summary", metavar="DIR", default=None,
+                    help="summarise the rocprofv3 runs under DIR (no GPU): write "
+                         "profiles/attn_traffic.json and print a markdown summary")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (scales the FETCH_SIZE / "
                          "WRITE_SIZE counters) and exit")
@@ -89,29 +97,132 @@ def cpu_baseline(wl, q, k, v, sample_rows: int):
     scale_rows = weight_all / weight_s
     full_s = (t1 - t0) + (t3 - t2) + ((t2 - t1) + (t4 - t3) + (t5 - t4)) * scale_rows
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                             None)
+    except OSError:
+        pass
     return {
         "value": round(full_s * 1e3, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+        "cpu_model": cpu_model, "host_cpus": os.cpu_count(),
         "sample": (f"pooling, last-block masses and budgets in full; proxy scores, lists and "
                    f"attention for {len(rows)} of {mq} block rows (all heads), scaled by causal "
                    f"work; measured {t5 - t0:.1f} s"),
     }
 
 
+# sources the attention kernel is compiled from
+KERNEL_SOURCES = ("attention.hip", "common.h", "internal.h")
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "attn_traffic.json")
+
+
+def kernel_sources_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2509_24745_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per sparse attention launch from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE runs (copy-calibrated), or None when the kernel
-    source has changed since they were taken."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "attn_traffic.json")
-    src = os.path.join(ROOT, "paper_2509_24745_amd", "csrc", "attention.hip")
+    sources have changed since they were taken."""
     try:
-        rec = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        rec = json.load(open(TRAFFIC_JSON))
+        sha = kernel_sources_sha256()
     except OSError:
         return None
-    if rec.get("attention_hip_sha256") != sha:
+    if rec.get("kernel_sources_sha256") != sha:
         return None
     return rec["fetch_bytes"] + rec["write_bytes"]
+
+
+# The rocprofv3 runs --profile-summary reads (DIR = their output folder).
+PROFILE_COMMANDS = [
+    "rocprofv3 --kernel-trace --stats -T -f csv -d DIR/trace -o run -- "
+    "python3 bench.py --steps 5 --warmup 2 --no-cpu-baseline",
+    "rocprofv3 --pmc FETCH_SIZE -T -f csv --kernel-include-regex attn_kernel -d DIR/pmc_FETCH_SIZE "
+    "-o run -- python3 bench.py --steps 1 --warmup 0 --no-dense --no-cpu-baseline",
+    "rocprofv3 --pmc WRITE_SIZE -T -f csv --kernel-include-regex attn_kernel -d DIR/pmc_WRITE_SIZE "
+    "-o run -- python3 bench.py --steps 1 --warmup 0 --no-dense --no-cpu-baseline",
+    "rocprofv3 --pmc FETCH_SIZE -T -f csv -d DIR/cal_FETCH_SIZE -o run -- "
+    "python3 bench.py --calibrate-copy",
+    "rocprofv3 --pmc WRITE_SIZE -T -f csv -d DIR/cal_WRITE_SIZE -o run -- "
+    "python3 bench.py --calibrate-copy",
+]
+
+
+def _kernel_label(name: str) -> str:
+    import re
+    m = re.match(r"_ZN2pa\d+(\w+?)I(DF16b|f)Li(\d+)E(?:Li(\d+)E)?(?:Lb([01])E)?", name)
+    if not m:
+        return name.split("(")[0][:48]
+    kind, t, a, b, flag = m.groups()
+    t = "bf16" if t == "DF16b" else "f32"
+    if kind == "attn_kernel":
+        return f"attn_kernel<{t},d{a},b{b},{'dense' if flag == '1' else 'sparse'}>"
+    if kind == "est_rowmax_kernel":
+        return f"est_rowmax_kernel<{t},d{a},b'{b}>"
+    return f"{kind}<{t},{a}>" if b is None else f"{kind}<{t},{a},{b}>"
+
+
+def profile_summary(d: str, workload: str) -> str:
+    """Summarise rocprofv3 output under `d` (the PROFILE_COMMANDS runs): write
+    profiles/attn_traffic.json and return a markdown summary."""
+    import csv
+    import glob
+
+    def rows(sub, pattern):
+        files = glob.glob(os.path.join(d, sub, pattern))
+        if not files:
+            raise SystemExit(f"no {pattern} under {os.path.join(d, sub)}")
+        with open(files[0]) as fh:
+            return list(csv.DictReader(fh))
+
+    def counter(sub, name, kernel_pred):
+        vals = [float(r["Counter_Value"]) for r in rows(sub, "*counter_collection.csv")
+                if r["Counter_Name"] == name and kernel_pred(r["Kernel_Name"])]
+        if not vals:
+            raise SystemExit(f"no {name} values in {sub}")
+        return sum(vals) / len(vals), len(vals)
+
+    sparse = lambda k: "attn_kernel" in k and "Lb0E" in k
+    copy = lambda k: "copy" in k.lower()
+    f_kib, nf = counter("pmc_FETCH_SIZE", "FETCH_SIZE", sparse)
+    w_kib, nw = counter("pmc_WRITE_SIZE", "WRITE_SIZE", sparse)
+    cf_kib, _ = counter("cal_FETCH_SIZE", "FETCH_SIZE", copy)
+    cw_kib, _ = counter("cal_WRITE_SIZE", "WRITE_SIZE", copy)
+    gib_kib = float(1 << 20)               # a 1 GiB copy reads and writes 2^20 KiB
+    f_scale, w_scale = gib_kib / cf_kib, gib_kib / cw_kib
+    fetch_b, write_b = f_kib * 1024 * f_scale, w_kib * 1024 * w_scale
+    rec = {"kernel": "attn_kernel<bf16,128,128,sparse>", "workload": workload,
+           "kernel_sources_sha256": kernel_sources_sha256(),
+           "fetch_bytes": fetch_b, "write_bytes": write_b, "fetch_kib": f_kib, "write_kib": w_kib,
+           "copy_fetch_kib_per_gib": cf_kib, "copy_write_kib_per_gib": cw_kib}
+    with open(TRAFFIC_JSON, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    stats = rows("trace", "*kernel_stats.csv")
+    out = ["## Kernel trace (rocprofv3 --kernel-trace --stats)", "",
+           "| kernel | calls | avg ms | min ms | max ms | % of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats:
+        out.append(f"| {_kernel_label(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e6:.3f} | "
+                   f"{float(r['MinNs']) / 1e6:.3f} | {float(r['MaxNs']) / 1e6:.3f} | "
+                   f"{float(r['Percentage']):.2f} |")
+    out += ["", "## HBM traffic of one sparse attention launch (rocprofv3 --pmc)", "",
+            "| counter | attn_kernel (KiB, mean of %d / %d launches) | 1 GiB copy (KiB) | scale | bytes per launch |" % (nf, nw),
+            "|---|---|---|---|---|",
+            f"| FETCH_SIZE | {f_kib:.0f} | {cf_kib:.1f} | {f_scale:.4f} | {fetch_b:.4e} |",
+            f"| WRITE_SIZE | {w_kib:.0f} | {cw_kib:.1f} | {w_scale:.4f} | {write_b:.4e} |",
+            "", f"Traffic per launch: {fetch_b + write_b:.4e} bytes.", "",
+            "Commands (repository root, one MI355X; DIR = the output folder):", ""]
+    out += ["    " + c for c in PROFILE_COMMANDS]
+    out += ["    python3 bench.py --profile-summary DIR"]
+    return "\n".join(out) + "\n"
 
 
 def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = True,
@@ -236,6 +347,95 @@ SWEEPS = {
 }
 
 
+def _stack_layer(job):
+    """Pool worker: draw layer `seed` of a stack and store its bf16 bits as .npy files."""
+    wname, seed, outdir = job
+    from paper_2509_24745_amd.synth import WORKLOADS, generate, to_bf16_bits
+    wl = WORKLOADS[wname].replace(seed=seed)
+    g = generate(wl)
+    paths = []
+    for x in ("q", "k", "v"):
+        path = os.path.join(outdir, f"layer{seed}_{x}.npy")
+        np.save(path, to_bf16_bits(g.pop(x)))
+        paths.append(path)
+    return seed, paths
+
+
+def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int, workers: int):
+    """A stack of `layers` layers of workload `wname`, layer l drawn with seed l.
+
+    Layers are generated by `workers` spawned processes (started before this
+    process touches the GPU), at most workers + 1 ahead of the GPU, and passed
+    through .npy files; each layer is timed like the default line (sparse path
+    and dense kernel), then the stack totals are printed.
+    """
+    import multiprocessing as mp
+    import shutil
+    import tempfile
+    from paper_2509_24745_amd.synth import WORKLOADS
+    base = WORKLOADS[wname]
+    if base.dtype != "bf16":
+        raise SystemExit("--stack runs bf16 workloads (layers pass as bf16 bits)")
+    layer_bytes = 2 * base.seq_len * (base.num_q_heads + 2 * base.num_kv_heads) * base.head_dim
+    tmp_root = None
+    if os.path.isdir("/dev/shm"):
+        st = os.statvfs("/dev/shm")
+        if st.f_bavail * st.f_frsize > (workers + 2) * layer_bytes * 1.2:
+            tmp_root = "/dev/shm"
+    outdir = tempfile.mkdtemp(prefix="proxyattn_stack_", dir=tmp_root)
+    pool = mp.get_context("spawn").Pool(workers)
+    sums = {"t_total": 0.0, "t_est": 0.0, "t_sel": 0.0, "t_attn": 0.0, "t_dense": 0.0, "blocks": 0,
+            "causal": 0}
+    try:
+        import torch
+        pending = {}
+        nxt = 0
+
+        def fill():
+            nonlocal nxt
+            while nxt < layers and len(pending) < workers + 1:
+                pending[nxt] = pool.apply_async(_stack_layer, ((wname, nxt, outdir),))
+                nxt += 1
+
+        fill()
+        for layer in range(layers):
+            seed, paths = pending.pop(layer).get()
+            fill()
+            bits = [np.load(p) for p in paths]
+            for p in paths:
+                os.remove(p)
+            inputs = tuple(torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+                           for a in bits)
+            del bits
+            wl = base.replace(seed=seed)
+            res, _, _ = measure(wl, steps, warmup, dense_steps, with_dense=True, inputs=inputs)
+            del inputs
+            line = summary_line(wl, res, steps)
+            line["layer"] = layer
+            print(json.dumps(line), flush=True)
+            sums["t_total"] += res["ms_total"]
+            sums["t_est"] += res["t_est"]
+            sums["t_sel"] += res["t_sel"]
+            sums["t_attn"] += res["t_attn"]
+            sums["t_dense"] += res["t_dense"]
+            sums["blocks"] += res["total_blocks"]
+            mq = wl.num_blocks
+            sums["causal"] += wl.num_q_heads * mq * (mq + 1) // 2
+    finally:
+        pool.terminate()
+        pool.join()
+        shutil.rmtree(outdir, ignore_errors=True)
+    f_dense = layers * 4.0 * base.num_q_heads * base.head_dim * base.seq_len * (base.seq_len + 1) / 2
+    print(json.dumps({
+        "stack": wname, "layers": layers, "t_total_ms": round(sums["t_total"], 3),
+        "t_estimate_ms": round(sums["t_est"], 3), "t_select_ms": round(sums["t_sel"], 3),
+        "t_attention_ms": round(sums["t_attn"], 3), "t_dense_ms": round(sums["t_dense"], 3),
+        "speedup_vs_dense": round(sums["t_dense"] / sums["t_total"], 3),
+        "dense_equiv_tflops": round(f_dense / (sums["t_total"] * 1e-3) / 1e12, 2),
+        "estimation_overhead_pct": round(100.0 * (sums["t_est"] + sums["t_sel"]) / sums["t_total"], 2),
+        "sparsity": round(1.0 - sums["blocks"] / sums["causal"], 4)}), flush=True)
+
+
 def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
     from paper_2509_24745_amd.synth import WORKLOADS
     cache = {}
@@ -262,6 +462,9 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU: --gpus must be 1 (the path shards "
                                    "by heads across GPUs only by design)"}))
         sys.exit(2)
+    if args.profile_summary:
+        print(profile_summary(args.profile_summary, args.workload), end="")
+        return
     import torch
     if args.calibrate_copy:
         n = 1 << 30
@@ -274,6 +477,10 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n}))
         return
     from paper_2509_24745_amd.synth import WORKLOADS
+    if args.stack:
+        run_stack(args.workload, args.stack, args.steps, args.warmup, args.dense_steps,
+                  args.stack_workers)
+        return
     if args.sweep:
         run_sweep(args.sweep, args.steps, args.warmup, args.dense_steps)
         return

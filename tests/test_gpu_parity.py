@@ -259,6 +259,47 @@ def test_empty_problem_is_a_noop():
     pa.proxyattn_dense_prefill(prob, None, None, None, None, None, None)
 
 
+def test_256k_layer_sampled_rows():
+    """One layer of the 256K stack (layer 0) in the benchmark's launch
+    configuration: pooled heads bit-exact, every head's last-block mass and
+    budget, and the proxy scores, lists and attention of seeded sampled query
+    rows (always including the last row) and their block rows."""
+    U = _gpu()
+    wl = WORKLOADS["llama3_8b_n262144"]
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    rng = np.random.default_rng(12345)
+    rows = np.unique(np.concatenate([rng.integers(0, wl.seq_len, 32), [wl.seq_len - 1]]))
+    brows = np.unique(rows // wl.block_size)
+    gpu = U.run_path(prob, q, k, v, wl.gamma)
+    sc = O.default_scale(wl.head_dim)
+    qg, kg = O.pool_proxy_heads(q, k, wl.num_proxy_groups, wl.stride, wl.dtype)
+    assert np.array_equal(gpu["qg"], qg) and np.array_equal(gpu["kg"], kg), "pooled heads differ"
+    oa, _ = O.proxy_block_logscore(qg, kg, wl.seq_len, wl.block_size, wl.stride, sc, rows=brows)
+    ga = gpu["logA"][:, brows]
+    ob = oa[:, brows]
+    assert np.array_equal(np.isneginf(ga), np.isneginf(ob)), "-inf pattern differs"
+    fin = np.isfinite(ob)
+    dla = float(np.max(np.abs(ga[fin] - ob[fin])))
+    assert dla <= LOGA_TOL, f"max |dlogA| = {dla}"
+    mass = O.lastblock_mass(q, k, wl.block_size, sc)
+    dm = float(np.max(np.abs(gpu["mass"] - mass))) / wl.block_size
+    assert dm <= MASS_RTOL, f"max |dmass|/rows = {dm}"
+    counts, cums = O.budget_counts(mass, wl.gamma, wl.min_budget_tokens, wl.block_size)
+    rep = C.Report()
+    C.check_counts(gpu["counts"], counts, cums, wl.gamma, wl.min_budget_tokens, wl.block_size, rep)
+    C.check_lists(gpu["block_count"], gpu["block_index"], oa, gpu["counts"], wl.num_q_heads,
+                  rows=brows, report=rep)
+    ref_out, ref_lse = O.block_sparse_attention(q, k, v, gpu["block_count"], gpu["block_index"],
+                                                wl.block_size, sc, query_rows=rows)
+    C.check_attention(gpu["out"][rows], ref_out[rows], rep)
+    dl = float(np.abs(gpu["lse"][:, rows] - ref_lse[:, rows]).max())
+    assert dl <= LSE_TOL, f"max |dlse| = {dl}"
+    print(f"\n[{wl.name}] |dlogA|={dla:.2e} |dmass|/rows={dm:.2e} max|dO|={rep.max_abs:.2e} "
+          f"mean|dO|={rep.mean_abs:.2e} |dlse|={dl:.2e} ambiguous heads={len(rep.ambiguous_heads)} "
+          f"rows={rep.ambiguous_rows} of {rep.rows_checked}", flush=True)
+
+
 @pytest.mark.parametrize("name,rows_per_head", [("llama3_8b_n32768", 256),
                                                 ("llama3_8b_n131072", 64)])
 def test_full_size_lists_and_sampled_attention(name, rows_per_head):
