@@ -349,10 +349,12 @@ SWEEPS = {
 
 def _stack_layer(job):
     """Pool worker: draw layer `seed` of a stack and store its bf16 bits as .npy files."""
-    wname, seed, outdir = job
+    wname, seed, outdir, threads = job
+    from threadpoolctl import threadpool_limits
     from paper_2509_24745_amd.synth import WORKLOADS, generate, to_bf16_bits
     wl = WORKLOADS[wname].replace(seed=seed)
-    g = generate(wl)
+    with threadpool_limits(threads):
+        g = generate(wl)
     paths = []
     for x in ("q", "k", "v"):
         path = os.path.join(outdir, f"layer{seed}_{x}.npy")
@@ -383,6 +385,7 @@ def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int
         if st.f_bavail * st.f_frsize > (workers + 2) * layer_bytes * 1.2:
             tmp_root = "/dev/shm"
     outdir = tempfile.mkdtemp(prefix="proxyattn_stack_", dir=tmp_root)
+    threads = max(1, (os.cpu_count() or workers) // workers)
     pool = mp.get_context("spawn").Pool(workers)
     sums = {"t_total": 0.0, "t_est": 0.0, "t_sel": 0.0, "t_attn": 0.0, "t_dense": 0.0, "blocks": 0,
             "causal": 0}
@@ -394,7 +397,7 @@ def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int
         def fill():
             nonlocal nxt
             while nxt < layers and len(pending) < workers + 1:
-                pending[nxt] = pool.apply_async(_stack_layer, ((wname, nxt, outdir),))
+                pending[nxt] = pool.apply_async(_stack_layer, ((wname, nxt, outdir, threads),))
                 nxt += 1
 
         fill()
