@@ -201,10 +201,24 @@ def budget_counts(mass: np.ndarray, gamma: float, min_budget_tokens: int, block_
 # --------------------------------------------------------------------------
 # Sec. 3.2, Eq. 3
 # --------------------------------------------------------------------------
-def select_blocks(logA: np.ndarray, counts: np.ndarray, num_q_heads: int, rows=None):
-    """Per head i and block row m: the min(count_i, m+1) causal blocks with
-    the highest shared score of the head's group (ties -> lower index),
-    listed in ascending order.
+def row_budget(count: int, m: int, nk: int, row_ratio: bool = False) -> int:
+    """Eq. 3's K = b_i N for block row m, with b_i = count / Nk.
+
+    Constant reading (N = Nk, the block-level sequence length): count blocks,
+    capped at the row's m+1 causal blocks.  Per-row-ratio reading (N = m+1):
+    ceil(b_i (m+1)) blocks, the same fraction of every row.
+    """
+    count = min(max(int(count), 0), nk)
+    if not row_ratio:
+        return min(count, m + 1)
+    return min(-(-count * (m + 1) // nk), m + 1)
+
+
+def select_blocks(logA: np.ndarray, counts: np.ndarray, num_q_heads: int, rows=None,
+                  row_ratio: bool = False):
+    """Per head i and block row m: the row_budget(count_i, m) causal blocks
+    with the highest shared score of the head's group (ties -> lower index),
+    listed in ascending order (Eq. 3).
 
     Returns (block_count [Hq, Mq] int32, block_index [Hq, Mq, Nk] int32, -1 pad).
     """
@@ -218,7 +232,7 @@ def select_blocks(logA: np.ndarray, counts: np.ndarray, num_q_heads: int, rows=N
             cand = np.arange(m + 1)
             order = np.lexsort((cand, -logA[g, m, :m + 1]))   # score desc, index asc
             for i in range(g * gsize, (g + 1) * gsize):
-                kk = min(int(counts[i]), m + 1)
+                kk = row_budget(counts[i], m, nk, row_ratio)
                 block_index[i, m, :kk] = np.sort(order[:kk])
                 block_count[i, m] = kk
     return block_count, block_index

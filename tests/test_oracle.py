@@ -306,6 +306,45 @@ def test_select_ties_go_to_lower_index_and_lists_nest():
         assert set(bi[0, m, :bc[0, m]]) <= set(bi[1, m, :bc[1, m]])
 
 
+def test_row_ratio_reading_matches_rational_definition_and_enumeration():
+    """Per-row-ratio reading of Eq. 3: K = ceil(b_i (m+1)) with b_i = count/Nk,
+    checked with exact rationals, and the lists against subset enumeration."""
+    from fractions import Fraction
+    rng = np.random.default_rng(12)
+    mq = 9
+    logA = np.full((1, mq, mq), -np.inf, np.float32)
+    for m in range(mq):
+        logA[0, m, :m + 1] = -rng.exponential(3.0, m + 1).astype(np.float32)
+    counts = np.array([1, 2, 4, 7, 9], np.int32)
+    bc, bi = O.select_blocks(logA, counts, 5, row_ratio=True)
+    for i, c in enumerate(counts):
+        for m in range(mq):
+            r = Fraction(int(c), mq) * (m + 1)
+            kk = -((-r.numerator) // r.denominator)        # ceil of the rational
+            assert bc[i, m] == kk == O.row_budget(c, m, mq, True)
+            assert 1 <= kk <= min(int(c), m + 1)
+            assert np.array_equal(bi[i, m, :kk], _brute_topk(logA[0, m, :m + 1], kk))
+            assert np.all(bi[i, m, kk:] == -1)
+        # the last row keeps the head's whole budget, as in the constant reading
+        assert bc[i, mq - 1] == c
+    # a full budget keeps every causal block in both readings
+    full, _ = O.select_blocks(logA, np.array([mq], np.int32), 1, row_ratio=True)
+    assert np.array_equal(full[0], np.arange(1, mq + 1))
+
+
+def test_static_topk_gives_every_head_of_a_group_the_same_lists():
+    rng = np.random.default_rng(13)
+    mq = 7
+    logA = np.full((2, mq, mq), -np.inf, np.float32)
+    for g in range(2):
+        for m in range(mq):
+            logA[g, m, :m + 1] = rng.standard_normal(m + 1).astype(np.float32)
+    bc, bi = O.select_blocks(logA, np.full(6, 3, np.int32), 6)
+    for i in (1, 2):
+        assert np.array_equal(bi[i], bi[0]) and np.array_equal(bi[3 + i], bi[3])
+    assert np.array_equal(bc[0], np.minimum(3, np.arange(1, mq + 1)))
+
+
 # ------------------------------------------------------ attention
 @pytest.mark.parametrize("n,b", [(256, 64), (200, 64), (50, 64)])
 def test_full_lists_reproduce_dense_causal_attention(n, b):
