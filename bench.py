@@ -47,7 +47,9 @@ def parse():
     ap.add_argument("--cpu-sample-rows", type=int, default=24,
                     help="block rows of the oracle sample (all heads)")
     ap.add_argument("--sweep", choices=["gamma_sigma_128k", "llama_32k", "qwen_64k",
-                                         "llama_256k_layer"], default=None,
+                                         "llama_256k_layer", "budget_variants_128k",
+                                         "stride_128k", "min_budget_128k", "groups_128k"],
+                    default=None,
                     help="print one JSON line per point of a workload sweep instead")
     ap.add_argument("--stack", type=int, default=None, metavar="LAYERS",
                     help="time a stack of LAYERS layers of --workload (layer l drawn with seed l; "
@@ -226,11 +228,19 @@ def profile_summary(d: str, workload: str) -> str:
 
 
 def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = True,
-            inputs=None):
+            inputs=None, variant: str = "dynamic", static_k: int | None = None,
+            dense_lse=None):
     """Time `steps` whole-path steps of workload `wl` (inputs resident in HBM).
 
-    Returns a dict of timings and derived figures; `inputs` may pass
-    already-uploaded (q, k, v) device tensors of the same shape.
+    `variant` selects the budget step (Alg. 1 and Eq. 3):
+      "dynamic"    proxyattn_select_budget (per-head budgets, constant reading);
+      "row_ratio"  proxyattn_budget + proxyattn_select_topk, per-row-ratio reading;
+      "static"     one budget of `static_k` blocks for every head
+                   (proxyattn_select_topk, constant reading; no budget step).
+    Returns (results, host arrays or None, device inputs).  With a dense
+    reference (`with_dense`, or `dense_lse` passed in) the results include
+    the attention-mass recall of the sparse lists, exp(lse_sparse - lse_dense)
+    per (head, row).
     """
     import torch
     from paper_2509_24745_amd import proxyattn as pa
@@ -251,13 +261,30 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
     q, k, v = inputs
     bufs = pa.Buffers(prob)
     stream = torch.cuda.current_stream()
+    if variant == "static":
+        bufs.head_count.fill_(int(static_k))
+        torch.cuda.synchronize()
+    elif variant not in ("dynamic", "row_ratio"):
+        raise ValueError(f"unknown variant {variant}")
+
+    def select():
+        if variant == "dynamic":
+            pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma,
+                                       wl.min_budget_tokens, bufs.head_count, bufs.block_count,
+                                       bufs.block_index, stream)
+            return
+        if variant == "row_ratio":
+            pa.proxyattn_budget(prob, bufs.mass, wl.gamma, wl.min_budget_tokens, bufs.head_count,
+                                stream)
+        mode = pa.TOPK_ROW_RATIO if variant == "row_ratio" else pa.TOPK_CONSTANT
+        pa.proxyattn_select_topk(prob, bufs.logscore, bufs.head_count, mode, bufs.block_count,
+                                 bufs.block_index, stream)
 
     def step(ev=None):
         if ev: ev[0].record(stream)
         pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, stream)
         if ev: ev[1].record(stream)
-        pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma, wl.min_budget_tokens,
-                                   bufs.head_count, bufs.block_count, bufs.block_index, stream)
+        select()
         if ev: ev[2].record(stream)
         pa.proxyattn_block_sparse_prefill(prob, q, k, v, bufs.block_count, bufs.block_index,
                                           bufs.out, bufs.lse, bufs.workspace, stream)
@@ -302,6 +329,17 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         torch.cuda.synchronize()
         t_dense = de[0].elapsed_time(de[1]) / dense_steps
         print(f"[bench] dense {t_dense:.3f} ms", file=sys.stderr, flush=True)
+        dense_lse = torch.empty_like(bufs.lse)
+        pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, dense_lse, bufs.workspace, stream)
+        torch.cuda.synchronize()
+        del dense_out
+    recall = None
+    if dense_lse is not None:
+        # share of each row's full causal attention mass inside its selected blocks
+        rec = torch.exp(bufs.lse - dense_lse).clamp_(max=1.0)
+        per_head = rec.mean(dim=1)
+        recall = {"mean": float(rec.mean()), "worst_head_mean": float(per_head.min()),
+                  "p01_row": float(torch.quantile(rec.flatten()[::97].float(), 0.01))}
     res = {
         "ms_total": ms_total, "t_est": t_est, "t_sel": t_sel, "t_attn": t_attn, "t_dense": t_dense,
         "sparsity": 1.0 - total_blocks / causal_blocks, "total_blocks": total_blocks,
@@ -310,6 +348,8 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         "head_count_max": int(counts.max()),
         "dense_mfma_frac": (4.0 * b * b * d * causal_blocks / (t_dense * 1e-3) / 1e12 / peak)
         if t_dense else None,
+        "variant": variant, "static_k": static_k, "recall": recall,
+        "head_count_mean": float(counts.mean()), "dense_lse": dense_lse,
     }
     return res, host, inputs
 
@@ -330,132 +370,60 @@ def summary_line(wl, r, steps):
         "dense_mfma_frac": round(r["dense_mfma_frac"], 4) if r["dense_mfma_frac"] else None,
         "head_count_min_median_max": [r["head_count_min"], r["head_count_median"],
                                       r["head_count_max"]],
+        "stride": wl.stride, "variant": r["variant"], "static_k": r["static_k"],
+        "recall": ({k: round(v, 5) for k, v in r["recall"].items()} if r["recall"] else None),
     }
 
 
+W128 = "llama3_8b_n131072"
 SWEEPS = {
     # the 128K layer over thresholds and head similarity
-    "gamma_sigma_128k": [("llama3_8b_n131072", dict(gamma=g, noise=s))
+    "gamma_sigma_128k": [(W128, dict(gamma=g, noise=s), "dynamic")
                          for s in (0.1, 0.3, 0.6) for g in (0.9, 0.95, 0.99)],
     # the 32K layer
-    "llama_32k": [("llama3_8b_n32768", {})],
+    "llama_32k": [("llama3_8b_n32768", {}, "dynamic")],
     # heterogeneous Qwen-shaped layer over proxy groups and minimum budgets
-    "qwen_64k": [("qwen25_7b_n65536", dict(num_proxy_groups=g, min_budget_tokens=mb))
+    "qwen_64k": [("qwen25_7b_n65536", dict(num_proxy_groups=g, min_budget_tokens=mb), "dynamic")
                  for g in (1, 2, 4, 7) for mb in (0, 2048)],
     # one layer of the 256K 32-layer stack (layer 0)
-    "llama_256k_layer": [("llama3_8b_n262144", {})],
+    "llama_256k_layer": [("llama3_8b_n262144", {}, "dynamic")],
+    # budget allocation at 128K: per-head dynamic budgets (constant and
+    # per-row-ratio readings of Eq. 3) against a static Top-K with the same
+    # mean budget, at three thresholds
+    "budget_variants_128k": [(W128, dict(gamma=g), v) for g in (0.9, 0.95, 0.99)
+                             for v in ("dynamic", "row_ratio", "static_match")],
+    # estimation stride, minimum budget and number of proxy heads at 128K
+    "stride_128k": [(W128, dict(stride=st), "dynamic") for st in (1, 2, 4)],
+    "min_budget_128k": [(W128, dict(min_budget_tokens=mb), "dynamic") for mb in (0, 1024, 2048)],
+    "groups_128k": [(W128, dict(num_proxy_groups=g), "dynamic") for g in (1, 2, 4, 8)],
 }
-
-
-def _stack_layer(job):
-    """Pool worker: draw layer `seed` of a stack and store its bf16 bits as .npy files."""
-    wname, seed, outdir, threads = job
-    from threadpoolctl import threadpool_limits
-    from paper_2509_24745_amd.synth import WORKLOADS, generate, to_bf16_bits
-    wl = WORKLOADS[wname].replace(seed=seed)
-    with threadpool_limits(threads):
-        g = generate(wl)
-    paths = []
-    for x in ("q", "k", "v"):
-        path = os.path.join(outdir, f"layer{seed}_{x}.npy")
-        np.save(path, to_bf16_bits(g.pop(x)))
-        paths.append(path)
-    return seed, paths
-
-
-def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int, workers: int):
-    """A stack of `layers` layers of workload `wname`, layer l drawn with seed l.
-
-    Layers are generated by `workers` spawned processes (started before this
-    process touches the GPU), at most workers + 1 ahead of the GPU, and passed
-    through .npy files; each layer is timed like the default line (sparse path
-    and dense kernel), then the stack totals are printed.
-    """
-    import multiprocessing as mp
-    import shutil
-    import tempfile
-    from paper_2509_24745_amd.synth import WORKLOADS
-    base = WORKLOADS[wname]
-    if base.dtype != "bf16":
-        raise SystemExit("--stack runs bf16 workloads (layers pass as bf16 bits)")
-    layer_bytes = 2 * base.seq_len * (base.num_q_heads + 2 * base.num_kv_heads) * base.head_dim
-    tmp_root = None
-    if os.path.isdir("/dev/shm"):
-        st = os.statvfs("/dev/shm")
-        if st.f_bavail * st.f_frsize > (workers + 2) * layer_bytes * 1.2:
-            tmp_root = "/dev/shm"
-    outdir = tempfile.mkdtemp(prefix="proxyattn_stack_", dir=tmp_root)
-    threads = max(1, (os.cpu_count() or workers) // workers)
-    pool = mp.get_context("spawn").Pool(workers)
-    sums = {"t_total": 0.0, "t_est": 0.0, "t_sel": 0.0, "t_attn": 0.0, "t_dense": 0.0, "blocks": 0,
-            "causal": 0}
-    try:
-        import torch
-        pending = {}
-        nxt = 0
-
-        def fill():
-            nonlocal nxt
-            while nxt < layers and len(pending) < workers + 1:
-                pending[nxt] = pool.apply_async(_stack_layer, ((wname, nxt, outdir, threads),))
-                nxt += 1
-
-        fill()
-        for layer in range(layers):
-            seed, paths = pending.pop(layer).get()
-            fill()
-            bits = [np.load(p) for p in paths]
-            for p in paths:
-                os.remove(p)
-            inputs = tuple(torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
-                           for a in bits)
-            del bits
-            wl = base.replace(seed=seed)
-            res, _, _ = measure(wl, steps, warmup, dense_steps, with_dense=True, inputs=inputs)
-            del inputs
-            line = summary_line(wl, res, steps)
-            line["layer"] = layer
-            print(json.dumps(line), flush=True)
-            sums["t_total"] += res["ms_total"]
-            sums["t_est"] += res["t_est"]
-            sums["t_sel"] += res["t_sel"]
-            sums["t_attn"] += res["t_attn"]
-            sums["t_dense"] += res["t_dense"]
-            sums["blocks"] += res["total_blocks"]
-            mq = wl.num_blocks
-            sums["causal"] += wl.num_q_heads * mq * (mq + 1) // 2
-    finally:
-        pool.terminate()
-        pool.join()
-        shutil.rmtree(outdir, ignore_errors=True)
-    f_dense = layers * 4.0 * base.num_q_heads * base.head_dim * base.seq_len * (base.seq_len + 1) / 2
-    print(json.dumps({
-        "stack": wname, "layers": layers, "t_total_ms": round(sums["t_total"], 3),
-        "t_estimate_ms": round(sums["t_est"], 3), "t_select_ms": round(sums["t_sel"], 3),
-        "t_attention_ms": round(sums["t_attn"], 3), "t_dense_ms": round(sums["t_dense"], 3),
-        "speedup_vs_dense": round(sums["t_dense"] / sums["t_total"], 3),
-        "dense_equiv_tflops": round(f_dense / (sums["t_total"] * 1e-3) / 1e12, 2),
-        "estimation_overhead_pct": round(100.0 * (sums["t_est"] + sums["t_sel"]) / sums["t_total"], 2),
-        "sparsity": round(1.0 - sums["blocks"] / sums["causal"], 4)}), flush=True)
 
 
 def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
     from paper_2509_24745_amd.synth import WORKLOADS
-    cache = {}
-    dense_cache = {}
-    for wname, kw in SWEEPS[name]:
+    cache = {}       # device inputs of the current generator settings
+    dense = {}       # dense time and lse per generator settings
+    last_mean = {}   # mean dynamic budget per (workload, settings) for static_match
+    for wname, kw, variant in SWEEPS[name]:
         wl = WORKLOADS[wname].replace(**kw) if kw else WORKLOADS[wname]
-        # inputs depend on the generator settings only (not on gamma, G, min budget)
+        # inputs depend on the generator settings only (not on gamma, G, stride, budgets)
         key = (wname, wl.structure, wl.seed)
-        dkey = (wname,)
-        res, host, inputs = measure(wl, steps, warmup, dense_steps,
-                                    with_dense=dkey not in dense_cache, inputs=cache.get(key))
+        static_k = None
+        if variant == "static_match":
+            variant = "static"
+            static_k = max(1, int(round(last_mean[(key, wl.gamma, wl.min_budget_tokens)])))
+        d = dense.get(key)
+        res, host, inputs = measure(wl, steps, warmup, dense_steps, with_dense=d is None,
+                                    inputs=cache.get(key), variant=variant, static_k=static_k,
+                                    dense_lse=d["lse"] if d else None)
         cache = {key: inputs}
-        if res["t_dense"] is None:
-            res["t_dense"] = dense_cache[dkey]["t_dense"]
-            res["dense_mfma_frac"] = dense_cache[dkey]["dense_mfma_frac"]
+        if d is None:
+            dense = {key: {"t": res["t_dense"], "frac": res["dense_mfma_frac"],
+                           "lse": res["dense_lse"]}}
         else:
-            dense_cache[dkey] = res
+            res["t_dense"], res["dense_mfma_frac"] = d["t"], d["frac"]
+        if variant == "dynamic":
+            last_mean[(key, wl.gamma, wl.min_budget_tokens)] = res["head_count_mean"]
         print(json.dumps(summary_line(wl, res, steps)), flush=True)
 
 
@@ -541,6 +509,8 @@ def main():
         if t_dense else None,
         "dense_mfma_frac": round(r["dense_mfma_frac"], 4) if t_dense else None,
         "computed_blocks": total_blocks,
+        "attention_mass_recall": ({k: round(x, 5) for k, x in r["recall"].items()}
+                                  if r["recall"] else None),
         "roofline": {"kernel": "attn_kernel (block-sparse prefill call)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),

@@ -145,6 +145,37 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
                             void* stream);
 
 /*
+ * Step 2 in two calls (budget variants; proxyattn_select_budget is
+ * proxyattn_budget followed by proxyattn_select_topk in constant mode).
+ *
+ * proxyattn_budget: Alg. 1's per-head budget alone; arguments as for
+ *     proxyattn_select_budget, head_count [Hq] int32 (out).
+ *
+ * proxyattn_select_topk: Eq. 3 with per-head budgets supplied by the caller
+ *     (device array head_count [Hq] int32, in; values outside [0, Nk] are
+ *     clamped to it), e.g. the output of proxyattn_budget, or one value for
+ *     every head (the static Top-K allocation the paper compares against in
+ *     its analysis of dynamic budgets, Sec. 5).  `mode` reads Eq. 3's
+ *     K = b_i N (b_i = head_count[i] / Nk):
+ *       PROXYATTN_TOPK_CONSTANT   N = Nk: every block row m keeps
+ *                                 min(head_count[i], m+1) blocks (the reading
+ *                                 proxyattn_select_budget uses);
+ *       PROXYATTN_TOPK_ROW_RATIO  N = m+1, the row's causal blocks: row m
+ *                                 keeps ceil(head_count[i] (m+1) / Nk) blocks.
+ *     Outputs as for proxyattn_select_budget (lists from the highest score
+ *     down, -1 padded).  Any other mode: PROXYATTN_E_INVALID.
+ */
+#define PROXYATTN_TOPK_CONSTANT 0
+#define PROXYATTN_TOPK_ROW_RATIO 1
+
+int proxyattn_budget(const proxyattn_problem* p, const float* lastblk_mass, float gamma,
+                     int32_t min_budget_tokens, int32_t* head_count, void* stream);
+
+int proxyattn_select_topk(const proxyattn_problem* p, const float* block_logscore,
+                          const int32_t* head_count, int32_t mode, int32_t* block_count,
+                          int32_t* block_index, void* stream);
+
+/*
  * Step 3: block-sparse causal attention.  For query token t in block m and
  * head i, out[t][i] = softmax_u(c * <q_t, k_u>) v_u over the keys u <= t of
  * the blocks block_index[i][m][0 .. block_count[i][m]).  Lists may be in any

@@ -79,13 +79,15 @@ def check_counts(gpu_counts, oracle_counts, oracle_cums, gamma, min_budget_token
 
 def check_lists(gpu_count, gpu_index, logA, counts_used, num_q_heads, rows=None,
                 report: Report | None = None, window: float = WINDOW,
-                rank_order: bool = True) -> Report:
+                rank_order: bool = True, row_ratio: bool = False) -> Report:
     """Verify GPU lists against the oracle's shared scores `logA` [G, Mq, Nk].
 
     Lists are compared as sets; with `rank_order` they must also be listed
     from the highest score down (the library's documented order).
-    `counts_used`: the per-head budget the GPU used (already validated).
+    `counts_used`: the per-head budget the GPU used (already validated);
+    `row_ratio`: the per-row-ratio reading of Eq. 3 sets each row's count.
     """
+    from oracle.proxyattn_oracle import row_budget
     report = report or Report()
     g_count, mq, nk = logA.shape
     gsize = num_q_heads // g_count
@@ -97,7 +99,7 @@ def check_lists(gpu_count, gpu_index, logA, counts_used, num_q_heads, rows=None,
             sc = logA[g, m, :m + 1].astype(np.float64)
             order = np.lexsort((np.arange(m + 1), -sc))
             for i in range(g * gsize, (g + 1) * gsize):
-                kk = min(int(counts_used[i]), m + 1)
+                kk = row_budget(counts_used[i], m, nk, row_ratio)
                 if int(gpu_count[i, m]) != kk:
                     raise ParityError(f"head {i} row {m}: count {int(gpu_count[i, m])} != {kk}")
                 lst_raw = gpu_index[i, m, :kk]

@@ -218,7 +218,44 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
     const int min_blocks = (int)(min_blocks64 > sh.mq ? sh.mq : min_blocks64);
     hipStream_t st = (hipStream_t)stream;
     PA_LAUNCH(launch_budget(sh, lastblk_mass, gamma, min_blocks, head_count, st), "budget");
-    PA_LAUNCH(launch_select(sh, block_logscore, head_count, block_count, block_index, st),
+    PA_LAUNCH(launch_select(sh, block_logscore, head_count, 0, block_count, block_index, st),
+              "select");
+    return PROXYATTN_OK;
+}
+
+int proxyattn_budget(const proxyattn_problem* p, const float* lastblk_mass, float gamma,
+                     int32_t min_budget_tokens, int32_t* head_count, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (!(gamma > 0.f && gamma <= 1.f))
+        return fail(PROXYATTN_E_INVALID, "gamma must lie in (0, 1]");
+    if (min_budget_tokens < 0) return fail(PROXYATTN_E_INVALID, "min_budget_tokens < 0");
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(lastblk_mass, "lastblk_mass"));
+    PA_TRY(check_ptr(head_count, "head_count"));
+    const int64_t min_blocks64 = ((int64_t)min_budget_tokens + sh.b - 1) / sh.b;
+    const int min_blocks = (int)(min_blocks64 > sh.mq ? sh.mq : min_blocks64);
+    PA_LAUNCH(launch_budget(sh, lastblk_mass, gamma, min_blocks, head_count, (hipStream_t)stream),
+              "budget");
+    return PROXYATTN_OK;
+}
+
+int proxyattn_select_topk(const proxyattn_problem* p, const float* block_logscore,
+                          const int32_t* head_count, int32_t mode, int32_t* block_count,
+                          int32_t* block_index, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (mode != PROXYATTN_TOPK_CONSTANT && mode != PROXYATTN_TOPK_ROW_RATIO)
+        return fail(PROXYATTN_E_INVALID, "unknown top-k mode %d", (int)mode);
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(block_logscore, "block_logscore"));
+    PA_TRY(check_ptr(head_count, "head_count"));
+    PA_TRY(check_ptr(block_count, "block_count"));
+    PA_TRY(check_ptr(block_index, "block_index"));
+    PA_LAUNCH(launch_select(sh, block_logscore, head_count, mode == PROXYATTN_TOPK_ROW_RATIO,
+                            block_count, block_index, (hipStream_t)stream),
               "select");
     return PROXYATTN_OK;
 }

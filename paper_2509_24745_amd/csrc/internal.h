@@ -69,7 +69,7 @@ hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float* par
 hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
-                         int* block_count, int* block_index, hipStream_t st);
+                         int row_ratio, int* block_count, int* block_index, hipStream_t st);
 // launch_kv_block also resets the attention work queues; launch_attention
 // must follow it on the same stream.
 hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,

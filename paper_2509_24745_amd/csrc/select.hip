@@ -9,7 +9,9 @@
 // select: one workgroup per (proxy group, block row m).  The m+1 causal
 //   candidates are sorted by (score descending, index ascending) as 64-bit
 //   keys in LDS (bitonic); every head of the group lists the first
-//   min(count_i, m+1) of them in that rank order and pads its row with -1.
+//   min(count_i, m+1) of them in that rank order and pads its row with -1
+//   (the per-row-ratio reading of Eq. 3 instead lists ceil(count_i (m+1) / Nk),
+//   i.e. the same fraction of every row's causal blocks).
 //   Rank order makes the lists of a group's heads prefixes of one another,
 //   so the attention workgroups of those heads, which run side by side on
 //   one XCD, fetch the same K/V blocks in the same order and share them
@@ -123,6 +125,7 @@ constexpr int kSelectThreads = 256;
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
                                                                 const float* __restrict__ logA,
                                                                 const int* __restrict__ head_count,
+                                                                int row_ratio,
                                                                 int* __restrict__ block_count,
                                                                 int* __restrict__ block_index) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
@@ -144,7 +147,10 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     // first min(count, m+1) of them (lists of one group are prefixes of
     // each other)
     for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
-        const int kk = min(head_count[i], ncand);
+        // counts outside [0, Nk] (caller-supplied) are clamped
+        const int c = min(max(head_count[i], 0), nk);
+        // per-row ratio: ceil(c (m+1) / Nk), exact in integers (< 2^26)
+        const int kk = row_ratio ? min((c * ncand + nk - 1) / nk, ncand) : min(c, ncand);
         int* out = block_index + ((int64_t)i * sh.mq + m) * nk;
         for (int p = tid; p < nk; p += kSelectThreads)
             out[p] = p < kk ? (int)(key[p] & 0xffffffffu) : -1;
@@ -160,7 +166,7 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
 }
 
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
-                         int* block_count, int* block_index, hipStream_t st) {
+                         int row_ratio, int* block_count, int* block_index, hipStream_t st) {
     const size_t smem = (size_t)next_pow2(sh.mq) * 8;
     if (smem > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
@@ -168,7 +174,7 @@ hipError_t launch_select(const Shape& sh, const float* logA, const int* head_cou
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(select_kernel, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh, logA,
-                       head_count, block_count, block_index);
+                       head_count, row_ratio, block_count, block_index);
     return hipGetLastError();
 }
 

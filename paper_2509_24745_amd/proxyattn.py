@@ -22,6 +22,7 @@ BF16 = 0
 F32 = 1
 
 E_OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, 1, 2, 3, 4
+TOPK_CONSTANT, TOPK_ROW_RATIO = 0, 1
 
 
 class proxyattn_problem(ctypes.Structure):
@@ -53,6 +54,10 @@ _SIGS = {
     "proxyattn_select_budget": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
                                 ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.c_void_p],
+    "proxyattn_budget": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float, ctypes.c_int32,
+                         ctypes.c_void_p, ctypes.c_void_p],
+    "proxyattn_select_topk": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
     "proxyattn_block_sparse_prefill": [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_dense_prefill": [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_error_string": [ctypes.c_int],
@@ -195,6 +200,21 @@ def proxyattn_select_budget(prob: Problem, block_logscore, lastblk_mass, gamma: 
     _check(lib().proxyattn_select_budget(ctypes.byref(p), _ptr(block_logscore), _ptr(lastblk_mass),
                                          float(gamma), int(min_budget_tokens), _ptr(head_count),
                                          _ptr(block_count), _ptr(block_index), _stream(stream)))
+
+
+def proxyattn_budget(prob: Problem, lastblk_mass, gamma: float, min_budget_tokens: int, head_count,
+                     stream=None):
+    p = prob.c_struct()
+    _check(lib().proxyattn_budget(ctypes.byref(p), _ptr(lastblk_mass), float(gamma),
+                                  int(min_budget_tokens), _ptr(head_count), _stream(stream)))
+
+
+def proxyattn_select_topk(prob: Problem, block_logscore, head_count, mode: int, block_count,
+                          block_index, stream=None):
+    p = prob.c_struct()
+    _check(lib().proxyattn_select_topk(ctypes.byref(p), _ptr(block_logscore), _ptr(head_count),
+                                       int(mode), _ptr(block_count), _ptr(block_index),
+                                       _stream(stream)))
 
 
 def proxyattn_block_sparse_prefill(prob: Problem, q, k, v, block_count, block_index, out, lse,

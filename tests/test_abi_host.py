@@ -129,11 +129,24 @@ def test_calls_reject_bad_arguments_before_launch():
         assert lib.proxyattn_select_budget(ctypes.byref(p), fake, fake, gamma, beta, fake, fake,
                                            fake, None) == pa.E_INVALID
     assert b"gamma" in lib.proxyattn_last_error() or b"min_budget" in lib.proxyattn_last_error()
+    for gamma, beta in ((0.0, 0), (1.5, 0), (float("nan"), 0), (0.9, -1)):
+        assert lib.proxyattn_budget(ctypes.byref(p), fake, gamma, beta, fake, None) == pa.E_INVALID
+    assert lib.proxyattn_budget(ctypes.byref(p), fake, 0.9, 0, None, None) == pa.E_INVALID
+    # unknown top-k mode, missing counts
+    for mode in (-1, 2, 7):
+        assert lib.proxyattn_select_topk(ctypes.byref(p), fake, fake, mode, fake, fake, None) \
+            == pa.E_INVALID
+    assert b"mode" in lib.proxyattn_last_error()
+    assert lib.proxyattn_select_topk(ctypes.byref(p), fake, None, pa.TOPK_CONSTANT, fake, fake,
+                                     None) == pa.E_INVALID
     # prefill without lists
     assert lib.proxyattn_block_sparse_prefill(ctypes.byref(p), fake, fake, fake, None, fake, fake,
                                               None, fake, ws, None) == pa.E_INVALID
     # empty problem: valid no-op, nothing touched
     p0 = _prob(seq_len=0).c_struct()
     assert lib.proxyattn_estimate(ctypes.byref(p0), None, None, None, None, None, 0, None) == 0
+    assert lib.proxyattn_budget(ctypes.byref(p0), None, 0.9, 0, None, None) == 0
+    assert lib.proxyattn_select_topk(ctypes.byref(p0), None, None, pa.TOPK_ROW_RATIO, None, None,
+                                     None) == 0
     assert lib.proxyattn_dense_prefill(ctypes.byref(p0), None, None, None, None, None, None, 0,
                                        None) == 0

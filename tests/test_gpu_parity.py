@@ -259,6 +259,51 @@ def test_empty_problem_is_a_noop():
     pa.proxyattn_dense_prefill(prob, None, None, None, None, None, None)
 
 
+def test_budget_and_topk_calls_and_budget_variants():
+    """proxyattn_budget + proxyattn_select_topk (constant reading) reproduce
+    proxyattn_select_budget bit for bit; the per-row-ratio reading and a
+    static Top-K match the oracle's selection; out-of-range counts clamp."""
+    U = _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    wl = LLAMA.replace(seq_len=8192 + 77)
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    mq = prob.num_blocks
+    ref = U.run_path(prob, q, k, None, wl.gamma)
+    qd, kd = U.to_dev(q, prob), U.to_dev(k, prob)
+    bufs = pa.Buffers(prob)
+    pa.proxyattn_estimate(prob, qd, kd, bufs.logscore, bufs.mass, bufs.workspace)
+    pa.proxyattn_budget(prob, bufs.mass, wl.gamma, 0, bufs.head_count)
+    pa.proxyattn_select_topk(prob, bufs.logscore, bufs.head_count, pa.TOPK_CONSTANT,
+                             bufs.block_count, bufs.block_index)
+    torch.cuda.synchronize()
+    assert np.array_equal(U.to_host(bufs.head_count), ref["counts"])
+    assert np.array_equal(U.to_host(bufs.block_count), ref["block_count"])
+    assert np.array_equal(U.to_host(bufs.block_index), ref["block_index"])
+    orc = _oracle(wl, q, k)
+    oa = orc["logA"]
+    # per-row-ratio reading on the GPU's budgets
+    pa.proxyattn_select_topk(prob, bufs.logscore, bufs.head_count, pa.TOPK_ROW_RATIO,
+                             bufs.block_count, bufs.block_index)
+    torch.cuda.synchronize()
+    counts = U.to_host(bufs.head_count)
+    rep = C.check_lists(U.to_host(bufs.block_count), U.to_host(bufs.block_index), oa, counts,
+                        wl.num_q_heads, row_ratio=True)
+    # static Top-K: one count for every head, and clamping of caller counts
+    static = np.full(wl.num_q_heads, 9, np.int32)
+    static[0], static[1] = -5, mq + 10
+    hc = torch.from_numpy(static).cuda()
+    pa.proxyattn_select_topk(prob, bufs.logscore, hc, pa.TOPK_CONSTANT, bufs.block_count,
+                             bufs.block_index)
+    torch.cuda.synchronize()
+    used = np.clip(static, 0, mq)
+    bc = U.to_host(bufs.block_count)
+    assert np.all(bc[0] == 0) and np.array_equal(bc[1], np.arange(1, mq + 1))
+    C.check_lists(bc, U.to_host(bufs.block_index), oa, used, wl.num_q_heads, report=rep)
+    print(f"\n[budget variants] ambiguous rows {rep.ambiguous_rows} of {rep.rows_checked}",
+          flush=True)
+
+
 def test_256k_layer_sampled_rows():
     """One layer of the 256K stack (layer 0) in the benchmark's launch
     configuration: pooled heads bit-exact, every head's last-block mass and
