@@ -48,7 +48,8 @@ def parse():
                     help="block rows of the oracle sample (all heads)")
     ap.add_argument("--sweep", choices=["gamma_sigma_128k", "llama_32k", "qwen_64k",
                                          "llama_256k_layer", "budget_variants_128k",
-                                         "stride_128k", "min_budget_128k", "groups_128k"],
+                                         "stride_128k", "min_budget_128k", "groups_128k",
+                                         "head_similarity_128k"],
                     default=None,
                     help="print one JSON line per point of a workload sweep instead")
     ap.add_argument("--stack", type=int, default=None, metavar="LAYERS",
@@ -396,7 +397,40 @@ SWEEPS = {
     "stride_128k": [(W128, dict(stride=st), "dynamic") for st in (1, 2, 4)],
     "min_budget_128k": [(W128, dict(min_budget_tokens=mb), "dynamic") for mb in (0, 1024, 2048)],
     "groups_128k": [(W128, dict(num_proxy_groups=g), "dynamic") for g in (1, 2, 4, 8)],
+    # head similarity (Eq. 4 overlap of the last token, top 1024) against the
+    # per-head deviation, beside the path's timing and recall
+    "head_similarity_128k": [(W128, dict(noise=sg), "dynamic+overlap") for sg in (0.1, 0.3, 0.6)],
 }
+
+
+def overlap_stats(wl, inputs, topk: int = 1024):
+    """Eq. 4 overlap matrices of the last query token on the GPU, summarised:
+    mean over pairs of different heads, split into pairs sharing a KV head
+    and pairs that do not; raw, sinks (4 tokens) removed, and renormalised."""
+    import torch
+    from paper_2509_24745_amd import proxyattn as pa
+    prob = pa.Problem(seq_len=wl.seq_len, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                      head_dim=wl.head_dim, block_size=wl.block_size,
+                      num_proxy_groups=wl.num_proxy_groups, stride=wl.stride, dtype=wl.dtype)
+    q, k, _ = inputs
+    ws = torch.empty(pa.proxyattn_workspace_size(prob), dtype=torch.uint8, device="cuda")
+    hq, rep = wl.num_q_heads, wl.num_q_heads // wl.num_kv_heads
+    scores = torch.empty((hq, hq), dtype=torch.float32, device="cuda")
+    grp = np.arange(hq) // rep
+    same = (grp[:, None] == grp[None, :]) & ~np.eye(hq, dtype=bool)
+    cross = grp[:, None] != grp[None, :]
+    out = {}
+    for tag, sink, renorm in (("raw", 0, False), ("no_sink", 4, False), ("no_sink_renorm", 4, True)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        pa.proxyattn_head_overlap(prob, q, k, wl.seq_len - 1, topk, sink, renorm, scores, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        sc = scores.cpu().numpy().astype(np.float64)
+        out[tag] = {"same_kv_mean": round(float(sc[same].mean()), 4),
+                    "cross_kv_mean": round(float(sc[cross].mean()), 4),
+                    "self_mean": round(float(np.diag(sc).mean()), 4), "ms": round(e0.elapsed_time(e1), 3)}
+    return out
 
 
 def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
@@ -409,6 +443,8 @@ def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
         # inputs depend on the generator settings only (not on gamma, G, stride, budgets)
         key = (wname, wl.structure, wl.seed)
         static_k = None
+        with_overlap = variant.endswith("+overlap")
+        variant = variant.replace("+overlap", "")
         if variant == "static_match":
             variant = "static"
             static_k = max(1, int(round(last_mean[(key, wl.gamma, wl.min_budget_tokens)])))
@@ -424,7 +460,10 @@ def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
             res["t_dense"], res["dense_mfma_frac"] = d["t"], d["frac"]
         if variant == "dynamic":
             last_mean[(key, wl.gamma, wl.min_budget_tokens)] = res["head_count_mean"]
-        print(json.dumps(summary_line(wl, res, steps)), flush=True)
+        line = summary_line(wl, res, steps)
+        if with_overlap:
+            line["head_overlap_top1024"] = overlap_stats(wl, inputs)
+        print(json.dumps(line), flush=True)
 
 
 def main():

@@ -197,6 +197,25 @@ int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const voi
                             const void* v, void* out, float* lse, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/*
+ * Head-similarity diagnostic (not on the prefill path): the overlap scores
+ * of Eq. 4 (the paper's sink-token analysis) for query token t =
+ * query_token, on every head's own full-resolution causal attention
+ * A[i][u] = softmax_u(c <q_t,i , k_u,kv(i)>), u <= t:
+ *     scores[i][j] = sum of A[j][u] over the topk tokens u with the largest
+ *                    A[i][u] (ties to the lower token; all t+1 tokens when
+ *                    topk > t+1).
+ *  sink_tokens in [0, query_token]: the attention to tokens u < sink_tokens
+ *      is set to zero first; renormalize (0 or 1): each head's remaining
+ *      attention is then rescaled to sum 1 (all zero if nothing remains).
+ *  scores: [Hq][Hq] fp32 device output.  workspace: as for
+ *  proxyattn_estimate (holds the probabilities).  Deterministic.
+ */
+int proxyattn_head_overlap(const proxyattn_problem* p, const void* q, const void* k,
+                           int32_t query_token, int32_t topk, int32_t sink_tokens,
+                           int32_t renormalize, float* scores, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
 /* Static text for a return code. */
 const char* proxyattn_error_string(int code);
 

@@ -3,7 +3,7 @@
 TEST INFRASTRUCTURE: imported only by the tests, the smoke check and the
 benchmark's CPU-baseline leg.
 
-Agreement required (the tolerances of the north-star specification):
+Agreement required (the parity bars of this path):
   * budgets: a head's block count may differ from the oracle's only where the
     cumulative-mass crossing of gamma is ambiguous, i.e. a count c is
     accepted when the oracle's sorted cumulative share satisfies

@@ -19,12 +19,17 @@ Sparse Attention via Representative Heads" (arXiv 2509.24745):
   select_blocks          Sec. 3.2, Eq. 3 (per-head Top-K over the shared score)
   block_sparse_attention Sec. 3.2, closing paragraph: causal attention over the
                          selected blocks only
+  head_overlap           Eq. 4 (the overlap scores of the sink-token analysis)
+                         and the Sec. 2.2 overlap measure it generalises
+  shared_ranking_curves  Sec. 2.2: cumulative attention of every head along
+                         the ranking by the head-mean attention and along its
+                         own ranking
 
 Arithmetic is fp32 (numpy float32), the precision the GPU kernels make their
 selection decisions in.  Inputs are fp32 arrays; bf16 problems pass values
 that are exactly bf16 (upcast losslessly).
 
-Readings of passages the paper leaves open (each is listed in the design doc):
+Readings of passages the paper leaves open:
   * pooling: fp32 sum over the group's heads in ascending head order, times
     fl32(1/|G|), rounded to nearest-even bf16 for bf16 problems.  The key of
     query head i is the key of its KV head, so for GQA the pooled key is the
@@ -318,3 +323,66 @@ def proxyattn_prefill(q, k, v, *, num_groups: int, block_size: int, stride: int,
     return dict(qg=qg, kg=kg, logA=logA, proxy_lse=proxy_lse, mass=mass, counts=counts,
                 cums=cums, block_count=block_count, block_index=block_index, out=out, lse=lse,
                 scale=sc)
+
+
+# --------------------------------------------------------------------------
+# Head-similarity diagnostics (Sec. 2.2 and the sink-token analysis, Eq. 4)
+# --------------------------------------------------------------------------
+def token_attention(q: np.ndarray, k: np.ndarray, t: int, scale: float) -> np.ndarray:
+    """Causal attention probabilities of query token t for every head at full
+    resolution: A [Hq, t+1] (fp32), head i against its KV head's keys."""
+    hq = q.shape[1]
+    rep = hq // k.shape[1]
+    a = np.empty((hq, t + 1), dtype=F32)
+    for i in range(hq):
+        s = F32(scale) * (k[:t + 1, i // rep] @ q[t, i])
+        e = np.exp(s - s.max())
+        a[i] = e / e.sum(dtype=F32)
+    return a
+
+
+def head_overlap(q: np.ndarray, k: np.ndarray, t: int, topk: int, scale: float,
+                 sink_tokens: int = 0, renormalize: bool = False) -> np.ndarray:
+    """Eq. 4: Score[i, j] = the attention head j gives to the top-k tokens of
+    head i (query token t; ties between equal scores go to the lower token).
+
+    ``sink_tokens``: the attention to the first n tokens is removed first
+    (set to zero); ``renormalize``: each head's remaining attention is then
+    rescaled to sum 1 (a head with nothing left stays all zero).
+    Returns Score [Hq, Hq] fp32 (sums taken in float64).
+    """
+    a = token_attention(q, k, t, scale)
+    if sink_tokens:
+        a[:, :sink_tokens] = 0.0
+    if renormalize:
+        tot = a.sum(axis=1, dtype=F32, keepdims=True)
+        a = np.where(tot > 0, a / np.where(tot > 0, tot, F32(1)), F32(0)).astype(F32)
+    hq, n1 = a.shape
+    kk = min(int(topk), n1)
+    tokens = np.arange(n1)
+    score = np.empty((hq, hq), dtype=F32)
+    for i in range(hq):
+        top = np.lexsort((tokens, -a[i]))[:kk]           # score desc, token asc
+        for j in range(hq):
+            score[i, j] = a[j, top].sum(dtype=np.float64)
+    return score
+
+
+def shared_ranking_curves(q: np.ndarray, k: np.ndarray, t: int, scale: float, points):
+    """Sec. 2.2: rank the tokens by their mean attention over the heads; for
+    every head, the cumulative attention of the first p tokens of that shared
+    ranking and of the head's own ranking, for p in ``points``.
+    Returns (shared [Hq, P], own [Hq, P]) in float64."""
+    a = token_attention(q, k, t, scale).astype(np.float64)
+    hq, n1 = a.shape
+    tokens = np.arange(n1)
+    shared_order = np.lexsort((tokens, -a.mean(axis=0)))
+    pts = [min(int(p), n1) for p in points]
+    shared = np.empty((hq, len(pts)))
+    own = np.empty((hq, len(pts)))
+    for i in range(hq):
+        cs = np.cumsum(a[i, shared_order])
+        co = np.cumsum(np.sort(a[i])[::-1])
+        shared[i] = [cs[p - 1] if p else 0.0 for p in pts]
+        own[i] = [co[p - 1] if p else 0.0 for p in pts]
+    return shared, own

@@ -117,7 +117,10 @@ WsLayout ws_layout(const Shape& sh) {
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.nchunks * sh.b * 2 * 4);
     L.kvb = off;  off = align_up(off + (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz);
     L.queue = off; off = align_up(off + (size_t)kNumXcd * kQueueStride * 4);
-    L.total = off;
+    // the diagnostic reuses the re-blocked K/V region (never live at the same time)
+    L.diag = L.kvb;
+    const size_t diag_end = L.diag + align_up((size_t)sh.hq * sh.n * 4) + align_up((size_t)sh.hq * 8);
+    L.total = off > diag_end ? off : diag_end;
     return L;
 }
 
@@ -319,4 +322,33 @@ const char* proxyattn_last_error(void) { return g_last_error; }
 
 const char* proxyattn_version(void) { return "0.1.0"; }
 
+int proxyattn_head_overlap(const proxyattn_problem* p, const void* q, const void* k,
+                           int32_t query_token, int32_t topk, int32_t sink_tokens,
+                           int32_t renormalize, float* scores, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (query_token < 0 || query_token >= sh.n)
+        return fail(PROXYATTN_E_INVALID, "query_token %d outside [0, %d)", (int)query_token, sh.n);
+    if (topk < 1) return fail(PROXYATTN_E_INVALID, "topk %d < 1", (int)topk);
+    if (sink_tokens < 0 || sink_tokens > query_token)
+        return fail(PROXYATTN_E_INVALID, "sink_tokens %d outside [0, query_token]", (int)sink_tokens);
+    if (renormalize != 0 && renormalize != 1)
+        return fail(PROXYATTN_E_INVALID, "renormalize must be 0 or 1");
+    PA_TRY(check_ptr(q, "q"));
+    PA_TRY(check_ptr(k, "k"));
+    PA_TRY(check_ptr(scores, "scores"));
+    WsLayout L;
+    PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
+    char* ws = (char*)workspace;
+    float* z = (float*)(ws + L.diag);
+    uint64_t* kth = (uint64_t*)(ws + L.diag + align_up((size_t)sh.hq * sh.n * 4));
+    PA_LAUNCH(launch_head_overlap(sh, q, k, query_token, topk, sink_tokens, renormalize, z, kth,
+                                  scores, (hipStream_t)stream),
+              "head_overlap");
+    return PROXYATTN_OK;
+}
+
 }  // extern "C"
+

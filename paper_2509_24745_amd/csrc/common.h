@@ -40,6 +40,16 @@ template <> __device__ __forceinline__ void put_elem<__bf16>(u32x4& x, int e, __
     x[e >> 1] |= (e & 1) ? (b << 16) : b;
 }
 
+// Element e of such a vector as a float.
+template <typename T> __device__ __forceinline__ float get_elem(const u32x4& x, int e);
+template <> __device__ __forceinline__ float get_elem<float>(const u32x4& x, int e) {
+    return __uint_as_float(x[e]);
+}
+template <> __device__ __forceinline__ float get_elem<__bf16>(const u32x4& x, int e) {
+    const uint32_t w = x[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+
 __device__ __forceinline__ u32x4 zero_u32x4() {
     u32x4 z = {0u, 0u, 0u, 0u};
     return z;

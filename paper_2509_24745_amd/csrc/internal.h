@@ -53,6 +53,8 @@ struct WsLayout {
     size_t part;     // last-block partial (max, sum) [Hq][nchunks][b][2] fp32
     size_t kvb;      // re-blocked K and V^T [Hkv][Mq][2 b d] (problem dtype)
     size_t queue;    // attention work-queue counters [kNumXcd][kQueueStride] int32
+    size_t diag;     // head-overlap diagnostic: probabilities [Hq][N] fp32, then the
+                     // per-head k-th keys [Hq] uint64 (overlaps kvb)
     size_t total;
 };
 
@@ -74,6 +76,9 @@ hipError_t launch_select(const Shape& sh, const float* logA, const int* head_cou
 // must follow it on the same stream.
 hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,
                            hipStream_t st);
+hipError_t launch_head_overlap(const Shape& sh, const void* q, const void* k, int t, int topk,
+                               int sink, int renorm, float* z, uint64_t* kth, float* score,
+                               hipStream_t st);
 hipError_t launch_attention(const Shape& sh, bool dense, const void* q, const void* kvb,
                             const int* block_count, const int* block_index, void* out, float* lse,
                             int* queue, hipStream_t st);

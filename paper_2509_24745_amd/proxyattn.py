@@ -58,6 +58,9 @@ _SIGS = {
                          ctypes.c_void_p, ctypes.c_void_p],
     "proxyattn_select_topk": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
+    "proxyattn_head_overlap": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                               ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                               ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_block_sparse_prefill": [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_dense_prefill": [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_error_string": [ctypes.c_int],
@@ -215,6 +218,16 @@ def proxyattn_select_topk(prob: Problem, block_logscore, head_count, mode: int, 
     _check(lib().proxyattn_select_topk(ctypes.byref(p), _ptr(block_logscore), _ptr(head_count),
                                        int(mode), _ptr(block_count), _ptr(block_index),
                                        _stream(stream)))
+
+
+def proxyattn_head_overlap(prob: Problem, q, k, query_token: int, topk: int, sink_tokens: int,
+                           renormalize: bool, scores, workspace, stream=None):
+    p = prob.c_struct()
+    _check(lib().proxyattn_head_overlap(ctypes.byref(p), _ptr(q), _ptr(k), int(query_token),
+                                        int(topk), int(sink_tokens), int(bool(renormalize)),
+                                        _ptr(scores), _ptr(workspace),
+                                        _nbytes(workspace) if workspace is not None else 0,
+                                        _stream(stream)))
 
 
 def proxyattn_block_sparse_prefill(prob: Problem, q, k, v, block_count, block_index, out, lse,

@@ -139,6 +139,16 @@ def test_calls_reject_bad_arguments_before_launch():
     assert b"mode" in lib.proxyattn_last_error()
     assert lib.proxyattn_select_topk(ctypes.byref(p), fake, None, pa.TOPK_CONSTANT, fake, fake,
                                      None) == pa.E_INVALID
+    # head-overlap diagnostic: token, k, sinks, renormalize flag, output
+    n = prob.seq_len
+    for t, kk, sink, rn in ((-1, 8, 0, 0), (n, 8, 0, 0), (5, 0, 0, 0), (5, 8, 6, 0), (5, 8, -1, 0),
+                            (5, 8, 0, 2)):
+        assert lib.proxyattn_head_overlap(ctypes.byref(p), fake, fake, t, kk, sink, rn, fake, fake,
+                                          ws, None) == pa.E_INVALID
+    assert lib.proxyattn_head_overlap(ctypes.byref(p), fake, fake, 5, 8, 0, 0, None, fake, ws,
+                                      None) == pa.E_INVALID
+    assert lib.proxyattn_head_overlap(ctypes.byref(p), fake, fake, 5, 8, 0, 0, fake, fake, ws - 1,
+                                      None) == pa.E_WORKSPACE
     # prefill without lists
     assert lib.proxyattn_block_sparse_prefill(ctypes.byref(p), fake, fake, fake, None, fake, fake,
                                               None, fake, ws, None) == pa.E_INVALID

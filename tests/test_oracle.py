@@ -413,3 +413,53 @@ def test_pipeline_sampled_rows_equal_full_run():
     assert np.allclose(full["out"][rows], part["out"][rows], rtol=0, atol=1e-6)
     for m in sorted(set(r // b for r in rows)):
         assert np.array_equal(full["block_index"][:, m], part["block_index"][:, m])
+
+
+# ------------------------------------------------------ head-similarity diagnostics (Eq. 4)
+def test_head_overlap_closed_forms():
+    """Q = 0 gives uniform attention 1/(t+1): Score = k/(t+1) everywhere; with
+    n sink tokens removed the top-k are tokens n..n+k-1 (the zeros rank last),
+    and renormalising scales every remaining token to 1/(t+1-n)."""
+    n, t, topk = 64, 40, 9
+    q = np.zeros((n, 4, 8), np.float32)
+    k = np.random.default_rng(3).standard_normal((n, 2, 8)).astype(np.float32)
+    s = O.head_overlap(q, k, t, topk, 0.3)
+    assert np.allclose(s, topk / (t + 1), atol=1e-6)
+    s = O.head_overlap(q, k, t, topk, 0.3, sink_tokens=4)
+    assert np.allclose(s, topk / (t + 1), atol=1e-6)
+    s = O.head_overlap(q, k, t, topk, 0.3, sink_tokens=4, renormalize=True)
+    assert np.allclose(s, topk / (t + 1 - 4), atol=1e-6)
+    # k beyond the visible tokens: every head's whole mass
+    assert np.allclose(O.head_overlap(q, k, t, 10 * n, 0.3), 1.0, atol=1e-6)
+
+
+def test_head_overlap_identical_heads_and_column_dominance():
+    rng = np.random.default_rng(4)
+    n, t, topk = 200, 150, 20
+    base = rng.standard_normal((n, 1, 16)).astype(np.float32)
+    q_same = np.repeat(base, 4, axis=1)
+    k = rng.standard_normal((n, 1, 16)).astype(np.float32)
+    s = O.head_overlap(q_same, k, t, topk, 0.5)
+    assert np.allclose(s, s[0, 0], atol=1e-6)              # every entry = the common top-k mass
+    q = rng.standard_normal((n, 6, 16)).astype(np.float32)
+    k2 = rng.standard_normal((n, 2, 16)).astype(np.float32)
+    s = O.head_overlap(q, k2, t, topk, 0.5)
+    a = O.token_attention(q, k2, t, 0.5).astype(np.float64)
+    for i in range(6):
+        # a head's own top-k holds the most of its mass of any k tokens ...
+        assert np.all(s[i, i] >= s[:, i] - 1e-6)
+        # ... which is the sum of its k largest probabilities (brute force)
+        assert abs(s[i, i] - np.sort(a[i])[::-1][:topk].sum()) < 1e-6
+
+
+def test_shared_ranking_curves_reduce_to_own_ranking_for_identical_heads():
+    rng = np.random.default_rng(5)
+    n, t = 128, 127
+    q = np.repeat(rng.standard_normal((n, 1, 8)).astype(np.float32), 3, axis=1)
+    k = rng.standard_normal((n, 1, 8)).astype(np.float32)
+    shared, own = O.shared_ranking_curves(q, k, t, 0.4, [1, 8, 64, 128])
+    assert np.allclose(shared, own, atol=1e-9)
+    assert np.allclose(own[:, -1], 1.0, atol=1e-6)
+    q2 = rng.standard_normal((n, 3, 8)).astype(np.float32)
+    shared, own = O.shared_ranking_curves(q2, k, t, 0.4, [1, 8, 64, 128])
+    assert np.all(shared <= own + 1e-12)                  # the own ranking is optimal

@@ -68,3 +68,25 @@ def test_named_workloads_are_consistent():
         assert wl.num_q_heads % wl.num_kv_heads == 0
         assert wl.num_q_heads % wl.num_proxy_groups == 0
         assert wl.block_size % wl.stride == 0
+
+
+def test_head_similarity_follows_the_deviation_knob():
+    """Eq. 4 overlap on the generator's heads: the mean overlap between
+    different heads falls as the per-head deviation sigma grows, with and
+    without the sink tokens (renormalised), the premise of proxy heads."""
+    from oracle import proxyattn_oracle as O
+    base = WORKLOADS["llama3_8b_n32768"].replace(seq_len=8192)
+    means = []
+    for sigma in (0.1, 0.3, 0.6):
+        wl = base.replace(noise=sigma)
+        g = generate(wl, with_v=False)
+        row = []
+        for sink, renorm in ((0, False), (4, True)):
+            s = O.head_overlap(g["q"], g["k"], wl.seq_len - 1, 1024, O.default_scale(wl.head_dim),
+                               sink_tokens=sink, renormalize=renorm).astype(np.float64)
+            off = s[~np.eye(s.shape[0], dtype=bool)]
+            row.append(off.mean())
+        means.append(row)
+    means = np.array(means)
+    assert np.all(np.diff(means, axis=0) < 0), means
+    assert means[0, 0] > 0.5, means
