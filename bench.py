@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--stack", type=int, default=None, metavar="LAYERS",
                     help="time a stack of LAYERS layers of --workload (layer l drawn with seed l; "
                          "one JSON line per layer, then the totals)")
+    ap.add_argument("--ttft", action="store_true",
+                    help="with --stack: add a decoder layer's non-attention work per layer and "
+                         "report the prefill time-to-first-token, sparse vs dense attention")
     ap.add_argument("--stack-workers", type=int, default=4,
                     help="processes generating stack layers ahead of the GPU")
     ap.add_argument("--profile-summary", metavar="DIR", default=None,
@@ -376,6 +379,166 @@ def summary_line(wl, r, steps):
     }
 
 
+def decoder_nonattn_ms(n: int, hidden: int = 4096, hq: int = 32, hkv: int = 8, d: int = 128,
+                       inter: int = 14336, reps: int = 3, rope_theta: float = 500000.0) -> float:
+    """Milliseconds of the non-attention work of one Llama-3-8B-shaped decoder
+    layer at n tokens in bf16 with random weights: RMSNorm, QKV projection,
+    RoPE on q and k, output projection, residual, RMSNorm, gate/up
+    projection, SiLU gate, down projection, residual.  Library GEMMs and
+    torch element-wise ops (the layer around the attention; the attention
+    itself is timed separately on structured inputs)."""
+    import torch
+    bf = torch.bfloat16
+    dev = "cuda"
+    g = torch.Generator(device=dev).manual_seed(0)
+    x = torch.randn(n, hidden, device=dev, dtype=bf, generator=g)
+    w_qkv = torch.randn(hidden, (hq + 2 * hkv) * d, device=dev, dtype=bf, generator=g) * hidden ** -0.5
+    w_o = torch.randn(hq * d, hidden, device=dev, dtype=bf, generator=g) * (hq * d) ** -0.5
+    w_gu = torch.randn(hidden, 2 * inter, device=dev, dtype=bf, generator=g) * hidden ** -0.5
+    w_dn = torch.randn(inter, hidden, device=dev, dtype=bf, generator=g) * inter ** -0.5
+    attn_out = torch.randn(n, hq * d, device=dev, dtype=bf, generator=g)
+    nrm1 = torch.ones(hidden, device=dev, dtype=bf)
+    nrm2 = torch.ones(hidden, device=dev, dtype=bf)
+    inv = 1.0 / (rope_theta ** (torch.arange(0, d, 2, device=dev, dtype=torch.float32) / d))
+    ang = torch.arange(n, device=dev, dtype=torch.float32)[:, None] * inv[None, :]
+    cos, sin = ang.cos().to(bf)[:, None, :], ang.sin().to(bf)[:, None, :]
+
+    def rms(t, w):
+        tf = t.float()
+        return (tf * torch.rsqrt(tf.pow(2).mean(-1, keepdim=True) + 1e-5)).to(bf) * w
+
+    def rope(t, heads):
+        t = t.reshape(n, heads, d)
+        a, b = t[..., : d // 2], t[..., d // 2:]
+        return torch.cat((a * cos - b * sin, b * cos + a * sin), dim=-1)
+
+    def layer():
+        h = rms(x, nrm1)
+        qkv = h @ w_qkv
+        rope(qkv[:, : hq * d], hq)
+        rope(qkv[:, hq * d:(hq + hkv) * d], hkv)
+        x2 = x + attn_out @ w_o
+        gu = rms(x2, nrm2) @ w_gu
+        a = torch.nn.functional.silu(gu[:, :inter]) * gu[:, inter:]
+        return x2 + a @ w_dn
+
+    layer()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        layer()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _stack_layer(job):
+    """Pool worker: draw layer `seed` of a stack and store its bf16 bits as .npy files."""
+    wname, seed, outdir, threads = job
+    from threadpoolctl import threadpool_limits
+    from paper_2509_24745_amd.synth import WORKLOADS, generate, to_bf16_bits
+    wl = WORKLOADS[wname].replace(seed=seed)
+    with threadpool_limits(threads):
+        g = generate(wl)
+    paths = []
+    for x in ("q", "k", "v"):
+        path = os.path.join(outdir, f"layer{seed}_{x}.npy")
+        np.save(path, to_bf16_bits(g.pop(x)))
+        paths.append(path)
+    return seed, paths
+
+
+def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int, workers: int,
+              ttft: bool = False):
+    """A stack of `layers` layers of workload `wname`, layer l drawn with seed l.
+
+    Layers are generated by `workers` spawned processes (started before this
+    process touches the GPU), at most workers + 1 ahead of the GPU, and passed
+    through .npy files; each layer is timed like the default line (sparse path
+    and dense kernel), then the stack totals are printed.  With `ttft`, the
+    totals add the non-attention work of a Llama-3-8B-shaped decoder layer
+    (decoder_nonattn_ms, timed once at this length) to every layer: a
+    prefill time-to-first-token with the sparse path vs dense attention.
+    """
+    import multiprocessing as mp
+    import shutil
+    import tempfile
+    from paper_2509_24745_amd.synth import WORKLOADS
+    base = WORKLOADS[wname]
+    if base.dtype != "bf16":
+        raise SystemExit("--stack runs bf16 workloads (layers pass as bf16 bits)")
+    layer_bytes = 2 * base.seq_len * (base.num_q_heads + 2 * base.num_kv_heads) * base.head_dim
+    tmp_root = None
+    if os.path.isdir("/dev/shm"):
+        st = os.statvfs("/dev/shm")
+        if st.f_bavail * st.f_frsize > (workers + 2) * layer_bytes * 1.2:
+            tmp_root = "/dev/shm"
+    outdir = tempfile.mkdtemp(prefix="proxyattn_stack_", dir=tmp_root)
+    threads = max(1, (os.cpu_count() or workers) // workers)
+    pool = mp.get_context("spawn").Pool(workers)
+    sums = {"t_total": 0.0, "t_est": 0.0, "t_sel": 0.0, "t_attn": 0.0, "t_dense": 0.0, "blocks": 0,
+            "causal": 0}
+    try:
+        import torch
+        pending = {}
+        nxt = 0
+
+        def fill():
+            nonlocal nxt
+            while nxt < layers and len(pending) < workers + 1:
+                pending[nxt] = pool.apply_async(_stack_layer, ((wname, nxt, outdir, threads),))
+                nxt += 1
+
+        fill()
+        for layer in range(layers):
+            seed, paths = pending.pop(layer).get()
+            fill()
+            bits = [np.load(p) for p in paths]
+            for p in paths:
+                os.remove(p)
+            inputs = tuple(torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+                           for a in bits)
+            del bits
+            wl = base.replace(seed=seed)
+            res, _, _ = measure(wl, steps, warmup, dense_steps, with_dense=True, inputs=inputs)
+            del inputs
+            line = summary_line(wl, res, steps)
+            line["layer"] = layer
+            print(json.dumps(line), flush=True)
+            sums["t_total"] += res["ms_total"]
+            sums["t_est"] += res["t_est"]
+            sums["t_sel"] += res["t_sel"]
+            sums["t_attn"] += res["t_attn"]
+            sums["t_dense"] += res["t_dense"]
+            sums["blocks"] += res["total_blocks"]
+            mq = wl.num_blocks
+            sums["causal"] += wl.num_q_heads * mq * (mq + 1) // 2
+        t_other = decoder_nonattn_ms(base.seq_len) if ttft else None
+    finally:
+        pool.terminate()
+        pool.join()
+        shutil.rmtree(outdir, ignore_errors=True)
+    f_dense = layers * 4.0 * base.num_q_heads * base.head_dim * base.seq_len * (base.seq_len + 1) / 2
+    if ttft:
+        t_sp = sums["t_total"] + layers * t_other
+        t_dn = sums["t_dense"] + layers * t_other
+        print(json.dumps({
+            "ttft_stack": wname, "layers": layers, "nonattn_ms_per_layer": round(t_other, 3),
+            "ttft_sparse_ms": round(t_sp, 1), "ttft_dense_ms": round(t_dn, 1),
+            "ttft_speedup": round(t_dn / t_sp, 3),
+            "attention_share_dense": round(sums["t_dense"] / t_dn, 3),
+            "attention_share_sparse": round(sums["t_total"] / t_sp, 3)}), flush=True)
+    print(json.dumps({
+        "stack": wname, "layers": layers, "t_total_ms": round(sums["t_total"], 3),
+        "t_estimate_ms": round(sums["t_est"], 3), "t_select_ms": round(sums["t_sel"], 3),
+        "t_attention_ms": round(sums["t_attn"], 3), "t_dense_ms": round(sums["t_dense"], 3),
+        "speedup_vs_dense": round(sums["t_dense"] / sums["t_total"], 3),
+        "dense_equiv_tflops": round(f_dense / (sums["t_total"] * 1e-3) / 1e12, 2),
+        "estimation_overhead_pct": round(100.0 * (sums["t_est"] + sums["t_sel"]) / sums["t_total"], 2),
+        "sparsity": round(1.0 - sums["blocks"] / sums["causal"], 4)}), flush=True)
+
+
 W128 = "llama3_8b_n131072"
 SWEEPS = {
     # the 128K layer over thresholds and head similarity
@@ -489,7 +652,7 @@ def main():
     from paper_2509_24745_amd.synth import WORKLOADS
     if args.stack:
         run_stack(args.workload, args.stack, args.steps, args.warmup, args.dense_steps,
-                  args.stack_workers)
+                  args.stack_workers, ttft=args.ttft)
         return
     if args.sweep:
         run_sweep(args.sweep, args.steps, args.warmup, args.dense_steps)
