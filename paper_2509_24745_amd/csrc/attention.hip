@@ -516,10 +516,11 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
 
 // Persistent kernel: one resident workgroup per slot (2B threads, B/32
 // waves); workgroup w takes the next item of queue w % 8 until the queue is
-// empty.  Taking work dynamically keeps every slot busy whatever the mix of
-// list lengths: the hardware dispatcher hands workgroups to the shader
-// engines of an XCD in a fixed rotation, so a grid of one workgroup per item
-// lets the engines that receive the long items hold back all the others.
+// empty, then helps drain the other queues.  Taking work dynamically keeps
+// every slot busy whatever the mix of list lengths: the hardware dispatcher
+// hands workgroups to the shader engines of an XCD in a fixed rotation, so a
+// grid of one workgroup per item lets the engines that receive the long items
+// hold back all the others.
 template <typename T, int D, int B, bool DENSE>
 __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __restrict__ q,
                                                         const T* __restrict__ kvb,
@@ -532,17 +533,24 @@ __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __res
     __shared__ __attribute__((aligned(16))) T ks_buf[2][C::K_ELEMS];
     __shared__ __attribute__((aligned(16))) T vs_buf[2][C::V_ELEMS];
     __shared__ int next_item;
-    const int x = blockIdx.x % kNumXcd;
     const int per_queue = attn_items(sh) / kNumXcd;
-    int* counter = queue + x * kQueueStride;
+    // own XCD's queue first; once it is empty, the other queues in turn
+    // (their remaining items are their shortest), so no XCD idles while
+    // another still has work.  Every probe of an empty queue moves on, so the
+    // loop ends after at most kNumXcd of them.
+    int x = blockIdx.x % kNumXcd, empty = 0;
     for (;;) {
         // the barrier also keeps the previous item's LDS reads ahead of the
         // next item's copies
-        if (threadIdx.x == 0) next_item = atomicAdd(counter, 1);
+        if (threadIdx.x == 0) next_item = atomicAdd(queue + x * kQueueStride, 1);
         __syncthreads();
         const int pos = next_item;
         __syncthreads();
-        if (pos >= per_queue) break;
+        if (pos >= per_queue) {
+            if (++empty == kNumXcd) break;
+            x = (x + 1) % kNumXcd;
+            continue;
+        }
         int m, i;
         if (!attn_item(sh, x + kNumXcd * pos, &m, &i)) continue;
         attn_one<T, D, B, DENSE>(sh, q, kvb, block_count, block_index, out, lse, m, i, ks_buf,
