@@ -64,6 +64,18 @@ CASES = {
     "llama_n100_single_partial_block": LLAMA.replace(seq_len=100),
     "fp32_d128_b128_n1000": LLAMA.replace(seq_len=1000, dtype="fp32", num_q_heads=8,
                                           num_kv_heads=2, num_proxy_groups=2),
+    # the remaining compiled (dtype, d, b) instantiations; b = 64 with d = 128
+    # is the two-wave workgroup at one wave per SIMD
+    "bf16_d128_b64_s4_n3100": LLAMA.replace(seq_len=3100, block_size=64, num_q_heads=16,
+                                            num_kv_heads=4, num_proxy_groups=2),
+    "bf16_d64_b128_n2600": Workload(name="t", seq_len=2600, num_q_heads=12, num_kv_heads=3,
+                                    head_dim=64, block_size=128, num_proxy_groups=3, stride=4,
+                                    dtype="bf16", gamma=0.95, structure=Structure(rank=8)),
+    "fp32_d64_b128_s2_n1500": Workload(name="t", seq_len=1500, num_q_heads=4, num_kv_heads=4,
+                                       head_dim=64, block_size=128, num_proxy_groups=1, stride=2,
+                                       dtype="fp32", gamma=0.9, structure=Structure(rank=8)),
+    "fp32_d128_b64_n700": LLAMA.replace(seq_len=700, dtype="fp32", block_size=64, num_q_heads=4,
+                                        num_kv_heads=1, num_proxy_groups=4),
 }
 
 
