@@ -271,28 +271,29 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
     elif variant not in ("dynamic", "row_ratio"):
         raise ValueError(f"unknown variant {variant}")
 
-    def select():
+    def select(st):
         if variant == "dynamic":
             pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma,
                                        wl.min_budget_tokens, bufs.head_count, bufs.block_count,
-                                       bufs.block_index, stream)
+                                       bufs.block_index, st)
             return
         if variant == "row_ratio":
             pa.proxyattn_budget(prob, bufs.mass, wl.gamma, wl.min_budget_tokens, bufs.head_count,
-                                stream)
+                                st)
         mode = pa.TOPK_ROW_RATIO if variant == "row_ratio" else pa.TOPK_CONSTANT
         pa.proxyattn_select_topk(prob, bufs.logscore, bufs.head_count, mode, bufs.block_count,
-                                 bufs.block_index, stream)
+                                 bufs.block_index, st)
 
-    def step(ev=None):
-        if ev: ev[0].record(stream)
-        pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, stream)
-        if ev: ev[1].record(stream)
-        select()
-        if ev: ev[2].record(stream)
+    def step(ev=None, st=None):
+        st = stream if st is None else st
+        if ev: ev[0].record(st)
+        pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, st)
+        if ev: ev[1].record(st)
+        select(st)
+        if ev: ev[2].record(st)
         pa.proxyattn_block_sparse_prefill(prob, q, k, v, bufs.block_count, bufs.block_index,
-                                          bufs.out, bufs.lse, bufs.workspace, stream)
-        if ev: ev[3].record(stream)
+                                          bufs.out, bufs.lse, bufs.workspace, st)
+        if ev: ev[3].record(st)
 
     for _ in range(warmup):
         step()
@@ -320,6 +321,32 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
     f_attn = 4.0 * b * b * d * total_blocks            # flops the sparse kernel computes
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
     achieved = f_attn / (t_attn * 1e-3) / 1e12
+    # the same step captured once in a HIP graph and replayed (no host launch work)
+    t_graph = None
+    ref_count = bufs.block_count.clone()
+    if steps > 0:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step(st=side)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(st=torch.cuda.current_stream())   # the capture stream
+        graph.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(steps):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        t_graph = g0.elapsed_time(g1) / steps
+        # a replay must reproduce the eager step (same buffers, deterministic kernels)
+        if not torch.equal(bufs.block_count, ref_count):
+            raise RuntimeError("graph replay differs from the eager step")
+        del graph
     t_dense = None
     if with_dense:
         de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -352,7 +379,7 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         "head_count_max": int(counts.max()),
         "dense_mfma_frac": (4.0 * b * b * d * causal_blocks / (t_dense * 1e-3) / 1e12 / peak)
         if t_dense else None,
-        "variant": variant, "static_k": static_k, "recall": recall,
+        "variant": variant, "static_k": static_k, "recall": recall, "t_graph": t_graph,
         "head_count_mean": float(counts.mean()), "dense_lse": dense_lse,
     }
     return res, host, inputs
@@ -702,6 +729,7 @@ def main():
         "t_estimate_ms": round(t_est, 4),
         "t_select_ms": round(t_sel, 4),
         "t_attention_ms": round(t_attn, 4),
+        "graph_replay_ms_per_step": round(r["t_graph"], 4) if r["t_graph"] else None,
         "dense_equiv_tflops": round(f_dense / (ms_total * 1e-3) / 1e12, 2),
         "estimation_overhead_pct": round(100.0 * (t_est + t_sel) / ms_total, 2),
         "sparsity": round(sparsity, 4),

@@ -352,6 +352,49 @@ def test_head_overlap_matches_oracle(case, t, topk, sink, renorm):
           flush=True)
 
 
+def test_whole_step_replays_from_a_hip_graph():
+    """estimate -> select_budget -> block_sparse_prefill captured once into a
+    HIP graph (the library issues no memsets, allocations or syncs) and
+    replayed three times, with eager work and synchronisations between the
+    replays: every replay reproduces the eager results bit for bit."""
+    U = _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    wl = LLAMA.replace(seq_len=4096 + 33)
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    qd, kd, vd = U.to_dev(q, prob), U.to_dev(k, prob), U.to_dev(v, prob)
+    bufs = pa.Buffers(prob)
+
+    def step():
+        pa.proxyattn_estimate(prob, qd, kd, bufs.logscore, bufs.mass, bufs.workspace)
+        pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma, 0, bufs.head_count,
+                                   bufs.block_count, bufs.block_index)
+        pa.proxyattn_block_sparse_prefill(prob, qd, kd, vd, bufs.block_count, bufs.block_index,
+                                          bufs.out, bufs.lse, bufs.workspace)
+
+    names = ("logscore", "mass", "head_count", "block_count", "block_index", "out", "lse")
+    step()
+    torch.cuda.synchronize()
+    ref = {n: getattr(bufs, n).clone() for n in names}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        for n in names:                       # eager work between the replays
+            getattr(bufs, n).zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(getattr(bufs, n), ref[n]), f"replay {rep}: {n} differs"
+
+
 def test_256k_layer_sampled_rows():
     """One layer of the 256K stack (layer 0) in the benchmark's launch
     configuration: pooled heads bit-exact, every head's last-block mass and
