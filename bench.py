@@ -231,6 +231,36 @@ def profile_summary(d: str, workload: str) -> str:
     return "\n".join(out) + "\n"
 
 
+def vendor_dense_ms(wl, inputs, reps: int = 2):
+    """torch's scaled_dot_product_attention restricted to its flash backend
+    (AOTriton on ROCm; no fallback to the quadratic-memory math path) on the
+    same Q/K/V, KV heads repeated for GQA: the vendor dense attention, for
+    context.  None if that backend is unavailable."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    q, k, v = inputs
+    rep = wl.num_q_heads // wl.num_kv_heads
+    qh = q.permute(1, 0, 2).unsqueeze(0).contiguous()
+    kh = k.permute(1, 0, 2).repeat_interleave(rep, dim=0).unsqueeze(0).contiguous()
+    vh = v.permute(1, 0, 2).repeat_interleave(rep, dim=0).unsqueeze(0).contiguous()
+    try:
+        with sdpa_kernel(SDPBackend.FLASH_ATTENTION):
+            f = lambda: torch.nn.functional.scaled_dot_product_attention(qh, kh, vh, is_causal=True)
+            f()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                f()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps
+    except RuntimeError:
+        return None
+    finally:
+        del qh, kh, vh
+
+
 def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = True,
             inputs=None, variant: str = "dynamic", static_k: int | None = None,
             dense_lse=None):
@@ -696,7 +726,10 @@ def main():
     if args.min_budget is not None:
         kw["min_budget_tokens"] = args.min_budget
     wl = wl.replace(**kw) if kw else wl
-    r, g, _ = measure(wl, args.steps, args.warmup, args.dense_steps, with_dense=not args.no_dense)
+    r, g, dev_inputs = measure(wl, args.steps, args.warmup, args.dense_steps,
+                               with_dense=not args.no_dense)
+    t_vendor = None if args.no_dense or wl.dtype != "bf16" else vendor_dense_ms(wl, dev_inputs)
+    del dev_inputs
     ms_total, t_est, t_sel, t_attn, t_dense = r["ms_total"], r["t_est"], r["t_sel"], r["t_attn"], r["t_dense"]
     n, hq, d, b = wl.seq_len, wl.num_q_heads, wl.head_dim, wl.block_size
     mq = wl.num_blocks
@@ -730,6 +763,8 @@ def main():
         "t_select_ms": round(t_sel, 4),
         "t_attention_ms": round(t_attn, 4),
         "graph_replay_ms_per_step": round(r["t_graph"], 4) if r["t_graph"] else None,
+        "torch_sdpa_flash_ms": round(t_vendor, 3) if t_vendor else None,
+        "speedup_vs_torch_sdpa_flash": round(t_vendor / ms_total, 3) if t_vendor else None,
         "dense_equiv_tflops": round(f_dense / (ms_total * 1e-3) / 1e12, 2),
         "estimation_overhead_pct": round(100.0 * (t_est + t_sel) / ms_total, 2),
         "sparsity": round(sparsity, 4),
