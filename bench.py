@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--sweep", choices=["gamma_sigma_128k", "llama_32k", "qwen_64k",
                                          "llama_256k_layer", "budget_variants_128k",
                                          "stride_128k", "min_budget_128k", "groups_128k",
-                                         "head_similarity_128k"],
+                                         "head_similarity_128k", "seq_len_llama"],
                     default=None,
                     help="print one JSON line per point of a workload sweep instead")
     ap.add_argument("--stack", type=int, default=None, metavar="LAYERS",
@@ -293,6 +293,10 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         dt = prob.torch_dtype
         inputs = tuple(torch.from_numpy(host[x]).to(dt).cuda() for x in ("q", "k", "v"))
     q, k, v = inputs
+    want_q = (wl.seq_len, wl.num_q_heads, wl.head_dim)
+    want_kv = (wl.seq_len, wl.num_kv_heads, wl.head_dim)
+    if tuple(q.shape) != want_q or tuple(k.shape) != want_kv or tuple(v.shape) != want_kv:
+        raise ValueError(f"inputs {tuple(q.shape)}/{tuple(k.shape)} do not match {wl.name}")
     bufs = pa.Buffers(prob)
     stream = torch.cuda.current_stream()
     if variant == "static":
@@ -617,6 +621,9 @@ SWEEPS = {
     "stride_128k": [(W128, dict(stride=st), "dynamic") for st in (1, 2, 4)],
     "min_budget_128k": [(W128, dict(min_budget_tokens=mb), "dynamic") for mb in (0, 1024, 2048)],
     "groups_128k": [(W128, dict(num_proxy_groups=g), "dynamic") for g in (1, 2, 4, 8)],
+    # the Llama-shaped layer over sequence lengths (same recipe and seed)
+    "seq_len_llama": [("llama3_8b_n32768", dict(seq_len=n, name=f"llama3_8b_n{n}"), "dynamic")
+                      for n in (8192, 16384, 32768, 65536, 131072, 262144)],
     # head similarity (Eq. 4 overlap of the last token, top 1024) against the
     # per-head deviation, beside the path's timing and recall
     "head_similarity_128k": [(W128, dict(noise=sg), "dynamic+overlap") for sg in (0.1, 0.3, 0.6)],
@@ -653,6 +660,15 @@ def overlap_stats(wl, inputs, topk: int = 1024):
     return out
 
 
+def input_key(wname: str, wl) -> tuple:
+    """Identity of a workload's generated inputs: every field that changes the
+    tensors (their shape and the generator settings), none that only changes
+    the method's arguments (gamma, G, stride, budgets).  Sweep points with equal
+    keys share one upload."""
+    return (wname, wl.seq_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.dtype,
+            wl.structure, wl.seed)
+
+
 def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
     from paper_2509_24745_amd.synth import WORKLOADS
     cache = {}       # device inputs of the current generator settings
@@ -660,8 +676,7 @@ def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
     last_mean = {}   # mean dynamic budget per (workload, settings) for static_match
     for wname, kw, variant in SWEEPS[name]:
         wl = WORKLOADS[wname].replace(**kw) if kw else WORKLOADS[wname]
-        # inputs depend on the generator settings only (not on gamma, G, stride, budgets)
-        key = (wname, wl.structure, wl.seed)
+        key = input_key(wname, wl)
         static_k = None
         with_overlap = variant.endswith("+overlap")
         variant = variant.replace("+overlap", "")

@@ -189,7 +189,59 @@ def proxyattn_workspace_layout(prob: Problem):
     return a.value, b.value
 
 
+# Size checks of torch arguments: the library receives raw pointers and
+# cannot see the allocations, so a tensor smaller than the problem would be
+# read or written out of bounds.  Each check needs the number of elements the
+# call touches from the tensor's data pointer (ints are raw pointers and are
+# passed through unchecked).
+def _need(x, n_elems: int, name: str, dtype=None):
+    if x is None or isinstance(x, int) or n_elems <= 0:
+        return
+    if dtype is not None and x.dtype != dtype:
+        raise ProxyAttnError(E_INVALID, f"{name}: dtype {x.dtype}, the problem needs {dtype}")
+    avail = x.untyped_storage().nbytes() // x.element_size() - x.storage_offset()
+    if avail < n_elems:
+        raise ProxyAttnError(E_INVALID, f"{name}: {avail} elements from its data pointer, the "
+                                        f"problem touches {n_elems}")
+
+
+def _span(n, heads, d, tok_stride, head_stride):
+    tok = tok_stride or heads * d
+    head = head_stride or d
+    return (n - 1) * tok + (heads - 1) * head + d if n > 0 else 0
+
+
+def _need_q(prob: Problem, q, name="q"):
+    _need(q, _span(prob.seq_len, prob.num_q_heads, prob.head_dim, prob.q_tok_stride,
+                   prob.q_head_stride), name, prob.torch_dtype)
+
+
+def _need_kv(prob: Problem, x, name):
+    _need(x, _span(prob.seq_len, prob.num_kv_heads, prob.head_dim, prob.kv_tok_stride,
+                   prob.kv_head_stride), name, prob.torch_dtype)
+
+
+def _need_out(prob: Problem, out):
+    _need(out, _span(prob.seq_len, prob.num_q_heads, prob.head_dim, prob.o_tok_stride,
+                     prob.o_head_stride), "out", prob.torch_dtype)
+
+
+def _need_scores(prob: Problem, block_logscore):
+    mq = prob.num_blocks
+    _need(block_logscore, prob.num_proxy_groups * mq * mq, "block_logscore", torch.float32)
+
+
+def _need_lists(prob: Problem, block_count, block_index):
+    mq = prob.num_blocks
+    _need(block_count, prob.num_q_heads * mq, "block_count", torch.int32)
+    _need(block_index, prob.num_q_heads * mq * mq, "block_index", torch.int32)
+
+
 def proxyattn_estimate(prob: Problem, q, k, block_logscore, lastblk_mass, workspace, stream=None):
+    _need_q(prob, q)
+    _need_kv(prob, k, "k")
+    _need_scores(prob, block_logscore)
+    _need(lastblk_mass, prob.num_q_heads * prob.num_blocks, "lastblk_mass", torch.float32)
     p = prob.c_struct()
     _check(lib().proxyattn_estimate(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(block_logscore),
                                     _ptr(lastblk_mass), _ptr(workspace), _nbytes(workspace)
@@ -199,6 +251,10 @@ def proxyattn_estimate(prob: Problem, q, k, block_logscore, lastblk_mass, worksp
 def proxyattn_select_budget(prob: Problem, block_logscore, lastblk_mass, gamma: float,
                             min_budget_tokens: int, head_count, block_count, block_index,
                             stream=None):
+    _need_scores(prob, block_logscore)
+    _need(lastblk_mass, prob.num_q_heads * prob.num_blocks, "lastblk_mass", torch.float32)
+    _need(head_count, prob.num_q_heads, "head_count", torch.int32)
+    _need_lists(prob, block_count, block_index)
     p = prob.c_struct()
     _check(lib().proxyattn_select_budget(ctypes.byref(p), _ptr(block_logscore), _ptr(lastblk_mass),
                                          float(gamma), int(min_budget_tokens), _ptr(head_count),
@@ -207,6 +263,8 @@ def proxyattn_select_budget(prob: Problem, block_logscore, lastblk_mass, gamma: 
 
 def proxyattn_budget(prob: Problem, lastblk_mass, gamma: float, min_budget_tokens: int, head_count,
                      stream=None):
+    _need(lastblk_mass, prob.num_q_heads * prob.num_blocks, "lastblk_mass", torch.float32)
+    _need(head_count, prob.num_q_heads, "head_count", torch.int32)
     p = prob.c_struct()
     _check(lib().proxyattn_budget(ctypes.byref(p), _ptr(lastblk_mass), float(gamma),
                                   int(min_budget_tokens), _ptr(head_count), _stream(stream)))
@@ -214,6 +272,9 @@ def proxyattn_budget(prob: Problem, lastblk_mass, gamma: float, min_budget_token
 
 def proxyattn_select_topk(prob: Problem, block_logscore, head_count, mode: int, block_count,
                           block_index, stream=None):
+    _need_scores(prob, block_logscore)
+    _need(head_count, prob.num_q_heads, "head_count", torch.int32)
+    _need_lists(prob, block_count, block_index)
     p = prob.c_struct()
     _check(lib().proxyattn_select_topk(ctypes.byref(p), _ptr(block_logscore), _ptr(head_count),
                                        int(mode), _ptr(block_count), _ptr(block_index),
@@ -222,6 +283,9 @@ def proxyattn_select_topk(prob: Problem, block_logscore, head_count, mode: int, 
 
 def proxyattn_head_overlap(prob: Problem, q, k, query_token: int, topk: int, sink_tokens: int,
                            renormalize: bool, scores, workspace, stream=None):
+    _need_q(prob, q)
+    _need_kv(prob, k, "k")
+    _need(scores, prob.num_q_heads * prob.num_q_heads, "scores", torch.float32)
     p = prob.c_struct()
     _check(lib().proxyattn_head_overlap(ctypes.byref(p), _ptr(q), _ptr(k), int(query_token),
                                         int(topk), int(sink_tokens), int(bool(renormalize)),
@@ -232,6 +296,12 @@ def proxyattn_head_overlap(prob: Problem, q, k, query_token: int, topk: int, sin
 
 def proxyattn_block_sparse_prefill(prob: Problem, q, k, v, block_count, block_index, out, lse,
                                    workspace, stream=None):
+    _need_q(prob, q)
+    _need_kv(prob, k, "k")
+    _need_kv(prob, v, "v")
+    _need_lists(prob, block_count, block_index)
+    _need_out(prob, out)
+    _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
     p = prob.c_struct()
     _check(lib().proxyattn_block_sparse_prefill(
         ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(block_count), _ptr(block_index),
@@ -240,6 +310,11 @@ def proxyattn_block_sparse_prefill(prob: Problem, q, k, v, block_count, block_in
 
 
 def proxyattn_dense_prefill(prob: Problem, q, k, v, out, lse, workspace, stream=None):
+    _need_q(prob, q)
+    _need_kv(prob, k, "k")
+    _need_kv(prob, v, "v")
+    _need_out(prob, out)
+    _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
     p = prob.c_struct()
     _check(lib().proxyattn_dense_prefill(
         ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(workspace),

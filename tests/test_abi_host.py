@@ -160,3 +160,32 @@ def test_calls_reject_bad_arguments_before_launch():
                                      None) == 0
     assert lib.proxyattn_dense_prefill(ctypes.byref(p0), None, None, None, None, None, None, 0,
                                        None) == 0
+
+
+def test_binding_rejects_tensors_smaller_than_the_problem():
+    """The library sees raw pointers only; the binding checks torch arguments
+    against the problem before any call (CPU tensors: nothing is launched)."""
+    import torch
+    _lib()
+    prob = _prob(seq_len=1000)
+    n, hq, hkv, d = prob.seq_len, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    mq = prob.num_blocks
+    bf = torch.bfloat16
+    q = torch.zeros(n, hq, d, dtype=bf)
+    k = torch.zeros(n, hkv, d, dtype=bf)
+    small_k = torch.zeros(n // 2, hkv, d, dtype=bf)
+    scores = torch.zeros(prob.num_proxy_groups, mq, mq)
+    mass = torch.zeros(hq, mq)
+    with pytest.raises(pa.ProxyAttnError, match="k: .* touches"):
+        pa.proxyattn_estimate(prob, q, small_k, scores, mass, None)
+    with pytest.raises(pa.ProxyAttnError, match="dtype"):
+        pa.proxyattn_estimate(prob, q.float(), k, scores, mass, None)
+    bc = torch.zeros(hq, mq, dtype=torch.int32)
+    bi64 = torch.zeros(hq, mq, mq, dtype=torch.int64)
+    with pytest.raises(pa.ProxyAttnError, match="block_index: dtype"):
+        pa.proxyattn_block_sparse_prefill(prob, q, k, k, bc, bi64, q, None, None)
+    # a view offset into a larger buffer counts only what lies past its start
+    big = torch.zeros(2 * n * hq * d, dtype=bf)
+    tail_view = big[n * hq * d + 1:]
+    with pytest.raises(pa.ProxyAttnError, match="out: .* touches"):
+        pa.proxyattn_dense_prefill(prob, q, k, k, tail_view, None, None)

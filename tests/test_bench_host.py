@@ -72,3 +72,19 @@ def test_profile_summary_scales_counters_by_the_copy_calibration(tmp_path, monke
     assert rec["write_bytes"] == pytest.approx(500.0 * 1024)
     assert rec["kernel_sources_sha256"] == bench.kernel_sources_sha256()
     assert "attn_kernel<bf16,d128,b128,sparse>" in md and "rocprofv3" in md
+
+
+def test_sweep_points_sharing_inputs_have_the_same_input_shapes():
+    """Sweep points reuse uploaded inputs only when their input key matches;
+    a key that ignored the sequence length once fed 8K tensors to a 16K
+    problem.  Equal keys must mean identical input shapes and draws."""
+    for name, points in bench.SWEEPS.items():
+        seen = {}
+        for wname, kw, _ in points:
+            wl = WORKLOADS[wname].replace(**kw) if kw else WORKLOADS[wname]
+            key = bench.input_key(wname, wl)
+            sig = (wl.seq_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.dtype,
+                   wl.structure, wl.seed)
+            assert seen.setdefault(key, sig) == sig, (name, key)
+    keys = {bench.input_key(w, WORKLOADS[w].replace(**kw)) for w, kw, _ in bench.SWEEPS["seq_len_llama"]}
+    assert len(keys) == len(bench.SWEEPS["seq_len_llama"])
