@@ -250,6 +250,27 @@ struct SubTileDma {
     }
 };
 
+// The two K and two V^T tiles in LDS.  They are four separate variables so
+// that each has an alias scope of its own: the compiler then sees that the
+// reads of one slot do not depend on the copy in flight into another, and
+// does not make them wait for it.
+template <typename T>
+struct LdsSlots {
+    T* k0;
+    T* k1;
+    T* v0;
+    T* v1;
+    __device__ __forceinline__ T* k(int p) const { return p ? k1 : k0; }
+    __device__ __forceinline__ T* v(int p) const { return p ? v1 : v0; }
+};
+
+// Waits for this wave's global -> LDS copies (they count in vmcnt, like any
+// vector-memory load).  A copy's data is in LDS only once its wave has
+// waited; the barrier after this wait then hands the tiles to the other
+// waves.  (s_waitcnt fields: vmcnt 0, expcnt and lgkmcnt left at their
+// maxima.)
+__device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Causal / ragged mask of one 64-key sub-tile: keys past `lim` (offset of
 // the last visible key inside the sub-tile) become -inf.  A key's offset is
 // 32 kt + 8 (r/4) + (r%4) + 4 h; the compile-time part is compared with the
@@ -321,8 +342,7 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
                                          const int* __restrict__ block_index,
                                          T* __restrict__ out, float* __restrict__ lse,
                                          const int m, const int i,
-                                         T (&ks_buf)[2][AttnCfg<T, D, B>::K_ELEMS],
-                                         T (&vs_buf)[2][AttnCfg<T, D, B>::V_ELEMS]) {
+                                         const LdsSlots<T>& slot) {
     typedef AttnCfg<T, D, B> C;
     typedef typename FragOf<T>::type Frag;
     typedef SubTileDma<T, D, C::KT, C::NTH / 64> Dma;
@@ -403,12 +423,13 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
     int nb0 = block_of(0);
     int nb1 = steps > 1 ? nb_of_step(1, nb0) : nb0;
     const Dma dma(w, lane);
-    dma.issue_k(sub_src(nb0, 0), ks_buf[0]);
-    dma.issue_v(sub_src(nb0, 0), vs_buf[0]);
-    if (steps > 1) dma.issue_k(sub_src(nb1, 1 % C::NSUB), ks_buf[1]);
+    dma.issue_k(sub_src(nb0, 0), slot.k(0));
+    dma.issue_v(sub_src(nb0, 0), slot.v(0));
+    if (steps > 1) dma.issue_k(sub_src(nb1, 1 % C::NSUB), slot.k(1));
+    wait_copies();
     __syncthreads();
     f32x16 s_cur[NT];
-    qk(s_cur, ks_buf[0]);
+    qk(s_cur, slot.k(0));
     if (needs_mask(nb0)) mask_tail<NT>(s_cur, qlim - nb0 * B, h);
     float mx = tile_max<NT>(s_cur) * sh.scale2;
 
@@ -418,13 +439,14 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
     auto step = [&](f32x16* sc, f32x16* sn, int st) {
         // K(st+1) and V(st) have landed; every wave is done with step st-1,
         // whose slots (K(st), V(st-1)) the next copies overwrite
+        wait_copies();
         __syncthreads();
         int nb2 = nb1;
         if (st + 2 < steps) {
             nb2 = nb_of_step(st + 2, nb1);
-            dma.issue_k(sub_src(nb2, (st + 2) % C::NSUB), ks_buf[st & 1]);
+            dma.issue_k(sub_src(nb2, (st + 2) % C::NSUB), slot.k(st & 1));
         }
-        if (st + 1 < steps) dma.issue_v(sub_src(nb1, (st + 1) % C::NSUB), vs_buf[(st + 1) & 1]);
+        if (st + 1 < steps) dma.issue_v(sub_src(nb1, (st + 1) % C::NSUB), slot.v((st + 1) & 1));
 
         // lazy rescaling: the reference max moves only when some row's max
         // exceeds it by more than kRescaleSlack (probabilities stay < 2^8)
@@ -443,7 +465,7 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
         // --- one basic block: scores of step st+1 (MFMA) interleaved with the
         // softmax of step st (VALU), then PV of step st (MFMA).  On the last
         // step the scores are computed from a stale slot and discarded.
-        qk(sn, ks_buf[(st + 1) & 1]);
+        qk(sn, slot.k((st + 1) & 1));
         Frag pf[NT][2];
 #pragma unroll
         for (int kt = 0; kt < NT; ++kt)
@@ -451,7 +473,7 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
             for (int r = 0; r < 16; ++r)
                 pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
         l_run += prob_sum<T, NT>(pf);
-        const T* vt_ = vs_buf[st & 1];
+        const T* vt_ = slot.v(st & 1);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -530,8 +552,11 @@ __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __res
                                                         float* __restrict__ lse,
                                                         int* __restrict__ queue) {
     typedef AttnCfg<T, D, B> C;
-    __shared__ __attribute__((aligned(16))) T ks_buf[2][C::K_ELEMS];
-    __shared__ __attribute__((aligned(16))) T vs_buf[2][C::V_ELEMS];
+    __shared__ __attribute__((aligned(16))) T ks0[C::K_ELEMS];
+    __shared__ __attribute__((aligned(16))) T ks1[C::K_ELEMS];
+    __shared__ __attribute__((aligned(16))) T vs0[C::V_ELEMS];
+    __shared__ __attribute__((aligned(16))) T vs1[C::V_ELEMS];
+    const LdsSlots<T> slot{ks0, ks1, vs0, vs1};
     __shared__ int next_item;
     const int per_queue = attn_items(sh) / kNumXcd;
     // own XCD's queue first; once it is empty, the other queues in turn
@@ -553,8 +578,7 @@ __global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __res
         }
         int m, i;
         if (!attn_item(sh, x + kNumXcd * pos, &m, &i)) continue;
-        attn_one<T, D, B, DENSE>(sh, q, kvb, block_count, block_index, out, lse, m, i, ks_buf,
-                                 vs_buf);
+        attn_one<T, D, B, DENSE>(sh, q, kvb, block_count, block_index, out, lse, m, i, slot);
     }
 }
 
