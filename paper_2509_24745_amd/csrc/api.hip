@@ -2,6 +2,7 @@
 // layout and kernel sequencing.  Every entry point validates all of its
 // arguments before enqueuing anything, never allocates and never
 // synchronises.
+#include <algorithm>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -82,7 +83,29 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     s.bp = p->block_size / p->stride;
     s.rep = p->num_q_heads / p->num_kv_heads;
     s.gsize = p->num_q_heads / p->num_proxy_groups;
-    s.nchunks = (p->seq_len + kMassChunk - 1) / kMassChunk;
+    // Key loops of the estimation kernels: one chunk per row (or per 2048
+    // keys) on long sequences; split further while a launch would have fewer
+    // than kFillGroups workgroups, so that short sequences do not leave most
+    // CUs idle behind a few long chains.
+    {
+        int mc = kMassChunk;
+        while (mc > s.b && (int64_t)s.hq * ((s.n + mc - 1) / mc) < kFillGroups) mc /= 2;
+        s.mass_chunk = mc;
+        s.nchunks = (s.n + mc - 1) / mc;
+        const int nrb = (s.np + 127) / 128, ntiles = (s.np + 31) / 32;
+        // workgroups of est_rowmax with kc tiles per chunk (counting stops at
+        // the target)
+        auto groups = [&](int kc) {
+            int64_t t = 0;
+            for (int x = 0; x < nrb && t * s.g < kFillGroups; ++x)
+                t += (std::min(x * 128 + 127, s.np - 1) / 32) / kc + 1;
+            return t * s.g;
+        };
+        int kc = std::max(4, (ntiles + 3) / 4 * 4);
+        while (kc > 4 && groups(kc) < kFillGroups) kc = std::max(4, (kc / 2 + 3) / 4 * 4);
+        s.est_kc = kc;
+        s.est_nc = std::max(1, (ntiles + kc - 1) / kc);
+    }
     s.scale = p->softmax_scale > 0.f ? p->softmax_scale : (float)(1.0 / sqrt((double)p->head_dim));
     s.scale2 = s.scale * 1.4426950408889634f;
     s.inv_gsize = 1.0f / (float)s.gsize;
@@ -112,7 +135,7 @@ WsLayout ws_layout(const Shape& sh) {
     size_t off = 0;
     L.qg = off;   off = align_up(off + (size_t)sh.g * sh.np * sh.d * esz);
     L.kg = off;   off = align_up(off + (size_t)sh.g * sh.np * sh.d * esz);
-    L.lse2 = off; off = align_up(off + (size_t)sh.g * sh.np * 4);
+    L.rowpart = off; off = align_up(off + (size_t)sh.g * sh.est_nc * sh.np * 8);
     L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.nchunks * sh.b * 2 * 4);
     L.kvb = off;  off = align_up(off + (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz);
@@ -194,8 +217,8 @@ int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
     char* ws = (char*)workspace;
     PA_LAUNCH(launch_pool(sh, q, k, ws + L.qg, ws + L.kg, st), "pool");
     PA_LAUNCH(launch_est_rowmax(sh, ws + L.qg, ws + L.kg, (float*)(ws + L.rbm),
-                                (float*)(ws + L.lse2), st), "est_rowmax");
-    PA_LAUNCH(launch_est_reduce(sh, (const float*)(ws + L.rbm), (const float*)(ws + L.lse2),
+                                (float2*)(ws + L.rowpart), st), "est_rowmax");
+    PA_LAUNCH(launch_est_reduce(sh, (const float*)(ws + L.rbm), (const float2*)(ws + L.rowpart),
                                 block_logscore, st), "est_reduce");
     PA_LAUNCH(launch_mass(sh, q, k, (float*)(ws + L.part), lastblk_mass, st), "mass");
     return PROXYATTN_OK;

@@ -10,10 +10,15 @@
 //
 // Proxy scores (a2 + a3):
 //   est_rowmax: one pass over the strided causal keys per strided query row,
-//     giving the row log2-sum-exp L2[t'] and, for every key block n <= m, the
-//     row's largest scaled logit in that block, rbm[m, n][t' - m b'].
-//   est_reduce: logA[m, n] = ln2 * max_{t' in m} (rbm[m, n][t'] - L2[t'])
-//     = log max_{t', u'} softmax(...)  (the max-pool of Eq. 1, log domain).
+//     giving, for every key block n <= m, the row's largest scaled logit in
+//     that block, rbm[m, n][t' - m b'], and the row's (max, sum of exp2)
+//     over the keys of each key chunk it covers.
+//   est_reduce: combines the chunks' (max, sum) pairs into the row
+//     log2-sum-exp L2[t'], then logA[m, n] = ln2 * max_{t' in m}
+//     (rbm[m, n][t'] - L2[t']) = log max_{t', u'} softmax(...)  (the
+//     max-pool of Eq. 1, log domain).
+// Long sequences use one chunk per row (the whole causal key range); short
+// ones split it so that the launch still fills the chip.
 // One MFMA pass instead of two (no recomputation of the tiles to re-derive
 // the max-pool after the row normaliser is known); rbm costs
 // G * Mq(Mq+1)/2 * b' * 4 bytes of workspace.
@@ -79,30 +84,35 @@ __device__ __forceinline__ f32x16 st_tile(const T* lds_tile, const typename Frag
 }
 
 // ---------------------------------------------------------------------------
-// a2: proxy row normaliser and per-(row, key block) max
-// grid (ceil(N'/128), G), 256 threads; workgroup x takes the strided rows
-// R0 = (gridDim.x - 1 - x) * 128 .. +127 (longest rows first), wave w rows
-// R0+32w..+31.  Only the wave's diagonal key tile needs the causal mask.
+// a2: per-(row, key block) max and per-(row, key chunk) (max, sum)
+// grid (ceil(N'/128), est_nc, G), 256 threads; workgroup (x, c) takes the
+// strided rows R0 = (gridDim.x - 1 - x) * 128 .. +127 (longest rows first),
+// wave w rows R0+32w..+31, against key tiles [c est_kc, (c+1) est_kc) of the
+// causal range (chunks past it exit at once).  Only the wave's diagonal key
+// tile needs the causal mask.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int BP>
 __global__ __launch_bounds__(256, 2) void est_rowmax_kernel(Shape sh, const T* __restrict__ qg,
                                                             const T* __restrict__ kg,
                                                             float* __restrict__ rbm,
-                                                            float* __restrict__ lse2) {
+                                                            float2* __restrict__ rowpart) {
     typedef typename FragOf<T>::type Frag;
     constexpr int KS = D / 16;
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, 256>::LDT];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
-    const int g = blockIdx.y;
+    const int c = blockIdx.y, g = blockIdx.z;
     const int np = sh.np;
     const int R0 = (gridDim.x - 1 - blockIdx.x) * 128;
+    const int kt_begin = c * sh.est_kc;
     const T* qbase = qg + (int64_t)g * np * D;
     const T* kbase = kg + (int64_t)g * np * D;
     const int row = R0 + 32 * w + lc;
     const bool wave_on = R0 + 32 * w < np;
     const int diag_tile = (R0 + 32 * w) / 32;   // the wave's rows all lie in this key tile
     const int wave_last_tile = wave_on ? diag_tile : -1;
-    const int last_tile = min(R0 + 127, np - 1) / 32;
+    const int last_row_tile = min(R0 + 127, np - 1) / 32;
+    if (kt_begin > last_row_tile) return;   // the whole workgroup: no barrier skipped
+    const int last_tile = min(last_row_tile, kt_begin + sh.est_kc - 1);
     const float scale2 = sh.scale2;
 
     Frag qf[KS];
@@ -117,10 +127,10 @@ __global__ __launch_bounds__(256, 2) void est_rowmax_kernel(Shape sh, const T* _
     // running max m (scaled, log2 units) and sum l of exp2(c' s - m)
     float m = kNegInf, l = 0.f, bm = kNegInf;
     KeyTile<T, D, 256> kt_ld;
-    kt_ld.load(kbase, D, 0, np, tid);
-    kt_ld.store(tiles[0], tid);
+    kt_ld.load(kbase, D, kt_begin * 32, np, tid);
+    kt_ld.store(tiles[kt_begin & 1], tid);
     __syncthreads();
-    for (int kt = 0; kt <= last_tile; ++kt) {
+    for (int kt = kt_begin; kt <= last_tile; ++kt) {
         if (kt < last_tile) kt_ld.load(kbase, D, (kt + 1) * 32, np, tid);
         if (kt <= wave_last_tile) {
             f32x16 acc = st_tile<T, D>(tiles[kt & 1], qf, lc, h);
@@ -170,25 +180,45 @@ __global__ __launch_bounds__(256, 2) void est_rowmax_kernel(Shape sh, const T* _
     const float mo = swap_halves(m), lo = swap_halves(l);
     const float mm = fmaxf(m, mo);
     if (h == 0 && row < np) {
-        // mm is finite (key 0 is visible to every row); a half with m = -inf has l = 0
+        // a half with m = -inf has l = 0; a row with no visible key in this
+        // chunk writes (-inf, 0)
         const float ll = (m == kNegInf ? 0.f : l * fast_exp2(m - mm)) +
                          (mo == kNegInf ? 0.f : lo * fast_exp2(mo - mm));
-        lse2[(int64_t)g * np + row] = mm + log2f(ll);
+        rowpart[((int64_t)g * sh.est_nc + c) * np + row] = make_float2(mm, ll);
     }
 }
 
 // ---------------------------------------------------------------------------
-// a3: block max-pool in the log domain.  grid (Mq, G), 256 threads.
+// a3: row normalisers and the block max-pool in the log domain.
+// grid (Mq, G), 256 threads.
 // ---------------------------------------------------------------------------
 template <int BP>
 __global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* __restrict__ rbm,
-                                                         const float* __restrict__ lse2,
+                                                         const float2* __restrict__ rowpart,
                                                          float* __restrict__ logA) {
     __shared__ float L[BP];
     const int m = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
     const int r0 = m * BP;
     const int nr = min(BP, sh.np - r0);
-    for (int j = tid; j < BP; j += 256) L[j] = j < nr ? lse2[(int64_t)g * sh.np + r0 + j] : 0.f;
+    // the block's rows lie in one 128-row band of est_rowmax (BP divides
+    // 128), which wrote chunks 0 .. nck-1 for them
+    const int nck = (min((r0 / 128) * 128 + 127, sh.np - 1) / 32) / sh.est_kc + 1;
+    for (int j = tid; j < BP; j += 256) {
+        float v = 0.f;
+        if (j < nr) {
+            const float2* pp = rowpart + (int64_t)g * sh.est_nc * sh.np + r0 + j;
+            float mx = kNegInf;
+            for (int cc = 0; cc < nck; ++cc) mx = fmaxf(mx, pp[(int64_t)cc * sh.np].x);
+            // mx is finite: key 0 (chunk 0) is visible to every row
+            float sum = 0.f;
+            for (int cc = 0; cc < nck; ++cc) {
+                const float2 x = pp[(int64_t)cc * sh.np];
+                if (x.x != kNegInf) sum += x.y * fast_exp2(x.x - mx);
+            }
+            v = mx + log2f(sum);
+        }
+        L[j] = v;
+    }
     __syncthreads();
     const int64_t tri_total = (int64_t)sh.mq * (sh.mq + 1) / 2;
     const float* base = rbm + ((int64_t)g * tri_total + tri_index(m, 0)) * BP;
@@ -231,7 +261,7 @@ __global__ __launch_bounds__(B * 2, 2) void mass_partial_kernel(Shape sh, const 
     const bool wave_on = 32 * w < nrows;
     const int wave_first_t = t0 + 32 * w;
     const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
-    const int key0 = c * kMassChunk, key1 = min(key0 + kMassChunk, n);
+    const int key0 = c * sh.mass_chunk, key1 = min(key0 + sh.mass_chunk, n);
     const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
     const T* kbase = k + (int64_t)kvh * sh.kv_head;
 
@@ -292,7 +322,7 @@ __global__ __launch_bounds__(B * 2, 2) void mass_final_kernel(Shape sh, const T*
                                                            float* __restrict__ mass) {
     typedef typename FragOf<T>::type Frag;
     constexpr int NTH = B * 2, NW = B / 32;
-    constexpr int BPC = kMassChunk / B;  // blocks per chunk
+    constexpr int BPC = kMassChunk / B;  // blocks per chunk, at most
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, NTH>::LDT];
     __shared__ float wpart[NW][BPC];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
@@ -304,7 +334,7 @@ __global__ __launch_bounds__(B * 2, 2) void mass_final_kernel(Shape sh, const T*
     const int wave_first_t = t0 + 32 * w;
     const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
     const bool wave_full = 32 * w + 31 < nrows;
-    const int key0 = c * kMassChunk, key1 = min(key0 + kMassChunk, n);
+    const int key0 = c * sh.mass_chunk, key1 = min(key0 + sh.mass_chunk, n);
     const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
     const int blk0 = key0 / B, nblk = (key1 - key0 + B - 1) / B;
     const T* kbase = k + (int64_t)kvh * sh.kv_head;
@@ -374,35 +404,35 @@ __global__ __launch_bounds__(B * 2, 2) void mass_final_kernel(Shape sh, const T*
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 static hipError_t rowmax_t(const Shape& sh, const void* qg, const void* kg, float* rbm,
-                           float* lse2, hipStream_t st) {
-    dim3 grid((sh.np + 127) / 128, sh.g);
+                           float2* rowpart, hipStream_t st) {
+    dim3 grid((sh.np + 127) / 128, sh.est_nc, sh.g);
     switch (sh.bp) {
-        case 16: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 16>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
-        case 32: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 32>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
-        case 64: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 64>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
-        case 128: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 128>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, lse2); break;
+        case 16: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 16>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
+        case 32: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 32>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
+        case 64: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 64>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
+        case 128: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 128>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
-                             float* lse2, hipStream_t st) {
+                             float2* rowpart, hipStream_t st) {
     if (sh.dtype == 0)
-        return sh.d == 64 ? rowmax_t<bf16, 64>(sh, qg, kg, rbm, lse2, st)
-                          : rowmax_t<bf16, 128>(sh, qg, kg, rbm, lse2, st);
-    return sh.d == 64 ? rowmax_t<float, 64>(sh, qg, kg, rbm, lse2, st)
-                      : rowmax_t<float, 128>(sh, qg, kg, rbm, lse2, st);
+        return sh.d == 64 ? rowmax_t<bf16, 64>(sh, qg, kg, rbm, rowpart, st)
+                          : rowmax_t<bf16, 128>(sh, qg, kg, rbm, rowpart, st);
+    return sh.d == 64 ? rowmax_t<float, 64>(sh, qg, kg, rbm, rowpart, st)
+                      : rowmax_t<float, 128>(sh, qg, kg, rbm, rowpart, st);
 }
 
-hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float* lse2, float* logA,
-                             hipStream_t st) {
+hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* rowpart,
+                             float* logA, hipStream_t st) {
     dim3 grid(sh.mq, sh.g);
     switch (sh.bp) {
-        case 16: hipLaunchKernelGGL((est_reduce_kernel<16>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
-        case 32: hipLaunchKernelGGL((est_reduce_kernel<32>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
-        case 64: hipLaunchKernelGGL((est_reduce_kernel<64>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
-        case 128: hipLaunchKernelGGL((est_reduce_kernel<128>), grid, dim3(256), 0, st, sh, rbm, lse2, logA); break;
+        case 16: hipLaunchKernelGGL((est_reduce_kernel<16>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
+        case 32: hipLaunchKernelGGL((est_reduce_kernel<32>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
+        case 64: hipLaunchKernelGGL((est_reduce_kernel<64>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
+        case 128: hipLaunchKernelGGL((est_reduce_kernel<128>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -23,7 +23,10 @@ struct Shape {
     int bp;       // b / s strided tokens per block
     int rep;      // Hq / Hkv
     int gsize;    // Hq / G
-    int nchunks;  // key chunks of the last-block mass kernels
+    int mass_chunk;  // keys per chunk of the last-block mass kernels
+    int nchunks;     // ceil(N / mass_chunk)
+    int est_kc;      // key tiles (32 keys) per chunk of est_rowmax, a multiple of 4
+    int est_nc;      // chunks of the longest row: ceil(ceil(N' / 32) / est_kc)
     float scale;  // softmax scale c
     float scale2; // c * log2(e)
     float inv_gsize;  // fl32(1 / |G|)
@@ -41,13 +44,18 @@ constexpr int kNumXcd = 8;
 // kNumXcd queues (one int32 counter per queue, each on its own 128-byte line).
 constexpr int kQueueStride = 32;
 
-// Keys per chunk of the last-block mass kernels (a multiple of every block size).
+// Largest key chunk of the last-block mass kernels (a multiple of every
+// block size); shorter sequences halve it down to one block.
 constexpr int kMassChunk = 2048;
+
+// Workgroups a launch of an estimation kernel should reach before its key
+// loops stop being split: 256 CUs x 2 resident workgroups x 2.
+constexpr int kFillGroups = 1024;
 
 // Byte offsets of the workspace regions (each 256-byte aligned).
 struct WsLayout {
     size_t qg, kg;   // pooled proxy heads [G][N'][d] (problem dtype)
-    size_t lse2;     // proxy row log2-sum-exp [G][N'] fp32
+    size_t rowpart;  // proxy rows' per-chunk (max, sum of exp2) [G][est_nc][N'] float2
     size_t rbm;      // per-(row, key block) max of the scaled proxy logits,
                      // [G][Mq(Mq+1)/2][b'] fp32 (lower-triangular block pairs)
     size_t part;     // last-block partial (max, sum) [Hq][nchunks][b][2] fp32
@@ -63,9 +71,9 @@ WsLayout ws_layout(const Shape& sh);
 hipError_t launch_pool(const Shape& sh, const void* q, const void* k, void* qg, void* kg,
                        hipStream_t st);
 hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
-                             float* lse2, hipStream_t st);
-hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float* lse2, float* logA,
-                             hipStream_t st);
+                             float2* rowpart, hipStream_t st);
+hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* rowpart,
+                             float* logA, hipStream_t st);
 hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float* part, float* mass,
                        hipStream_t st);
 hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,

@@ -98,14 +98,58 @@ def test_bad_struct_size_and_null_problem():
     assert lib.proxyattn_workspace_size(None, ctypes.byref(n)) == pa.E_INVALID
 
 
-def test_workspace_size_formula_and_empty_problem():
+def _key_chunks(n, hq, g, b, s):
+    """The library's rule for splitting the estimation kernels' key loops:
+    halve the mass kernels' 2048-key chunk (not below one block), and the
+    block-scoring chunk of 32-key tiles (a multiple of 4, not below 4), while
+    a launch has fewer than 1024 workgroups.  Returns (mass chunk, mass
+    chunks, tiles per scoring chunk, scoring chunks of the longest row)."""
+    npr = -(-n // s)
+    mc = 2048
+    while mc > b and hq * -(-n // mc) < 1024:
+        mc //= 2
+    nrb, nt = -(-npr // 128), -(-npr // 32)
+
+    def groups(kc):
+        return g * sum((min(x * 128 + 127, npr - 1) // 32) // kc + 1 for x in range(nrb))
+
+    kc = max(4, -(-nt // 4) * 4)
+    while kc > 4 and groups(kc) < 1024:
+        kc = max(4, -(-(kc // 2) // 4) * 4)
+    return mc, -(-n // mc), kc, max(1, -(-nt // kc))
+
+
+def test_key_chunk_rule():
+    # long sequences keep one scoring chunk per row and 2048-key mass chunks
+    assert _key_chunks(131072, 32, 4, 128, 4) == (2048, 64, 1024, 1)
+    assert _key_chunks(262144, 32, 4, 128, 4) == (2048, 128, 2048, 1)
+    # short ones split until the launches reach 1024 workgroups (or the floor)
+    assert _key_chunks(32768, 32, 4, 128, 4) == (1024, 32, 32, 8)
+    assert _key_chunks(8192, 32, 4, 128, 4) == (256, 32, 4, 16)
+    assert _key_chunks(2048, 32, 4, 128, 4) == (128, 16, 4, 4)
+
+
+@pytest.mark.parametrize("n,hq,hkv,g,b,s", [
+    (32768, 32, 8, 4, 128, 4), (8192, 32, 8, 4, 128, 4), (131072, 32, 8, 4, 128, 4),
+    (65536, 28, 4, 2, 128, 4), (3000, 8, 2, 2, 64, 2), (777, 4, 4, 1, 64, 1)])
+def test_workspace_size_formula(n, hq, hkv, g, b, s):
     _lib()
-    prob = _prob(seq_len=32768)
-    g, npr, d, mq, bp = 4, 8192, 128, 256, 32
-    expect_min = 2 * g * npr * d * 2 + g * npr * 4 + g * (mq * (mq + 1) // 2) * bp * 4 \
-        + 32 * 16 * 128 * 2 * 4 + 8 * mq * 2 * d * 128 * 2 + 8 * 32 * 4
-    ws = pa.proxyattn_workspace_size(prob)
-    assert expect_min <= ws <= expect_min + 7 * 256
+    d = 128
+    prob = _prob(seq_len=n, num_q_heads=hq, num_kv_heads=hkv, num_proxy_groups=g,
+                 block_size=b, stride=s)
+    npr, mq, bp = -(-n // s), -(-n // b), b // s
+    _, nchunks, _, est_nc = _key_chunks(n, hq, g, b, s)
+    regions = [g * npr * d * 2, g * npr * d * 2, g * est_nc * npr * 8,
+               g * (mq * (mq + 1) // 2) * bp * 4, hq * nchunks * b * 2 * 4,
+               hkv * mq * 2 * d * b * 2, 8 * 32 * 4]
+    end = sum(-(-r // 256) * 256 for r in regions)
+    kvb = sum(-(-r // 256) * 256 for r in regions[:5])
+    diag_end = kvb + -(-(hq * n * 4) // 256) * 256 + -(-(hq * 8) // 256) * 256
+    assert pa.proxyattn_workspace_size(prob) == max(end, diag_end)
+
+
+def test_workspace_size_of_empty_problem():
+    _lib()
     assert pa.proxyattn_workspace_size(_prob(seq_len=0)) == 0
 
 
