@@ -125,11 +125,16 @@ TRAFFIC_JSON = os.path.join(ROOT, "profiles", "attn_traffic.json")
 
 
 def kernel_sources_sha256() -> str:
+    """Hash of the attention kernel's sources with // comments and
+    whitespace removed, so that only a change to the code itself marks the
+    committed traffic counters as stale."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2509_24745_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2509_24745_amd", "csrc", f), encoding="utf-8") as fh:
+            code = re.sub(r"//[^\n]*", "", fh.read())
+        h.update(re.sub(r"\s+", "", code).encode())
     return h.hexdigest()
 
 

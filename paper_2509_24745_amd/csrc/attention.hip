@@ -27,9 +27,10 @@
 //     during step j the copies of K(j+2) and V(j+1) run while the wave reads
 //     K(j+1) and V(j);
 //   - the scores of step j+1 (MFMA) are interleaved instruction by
-//     instruction with the softmax of step j (VALU) in one basic block, then
-//     PV of step j runs; the row max of step j+1 closes the step, so the
-//     rare rescale branch stays out of that block.
+//     instruction with the softmax of step j (VALU), then PV of step j runs,
+//     as one explicit software pipeline in which every LDS fragment read is
+//     issued two MFMAs ahead of its use; the row max of step j+1 closes the
+//     step, so the rare rescale branch stays out of that block.
 #include <algorithm>
 #include <mutex>
 #include <vector>
@@ -271,6 +272,10 @@ struct LdsSlots {
 // maxima.)
 __device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// MFMAs between the LDS read of an operand fragment and the MFMA that uses it
+// (bf16 attention loop).
+constexpr int kReadLead = 2;
+
 // Causal / ragged mask of one 64-key sub-tile: keys past `lim` (offset of
 // the last visible key inside the sub-tile) become -inf.  A key's offset is
 // 32 kt + 8 (r/4) + (r%4) + 4 h; the compile-time part is compared with the
@@ -462,43 +467,74 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
         // probabilities are exp2(-inf) = 0
         const float neg_m = (m_run == kNegInf) ? 0.f : -m_run;
 
-        // --- one basic block: scores of step st+1 (MFMA) interleaved with the
-        // softmax of step st (VALU), then PV of step st (MFMA).  On the last
-        // step the scores are computed from a stale slot and discarded.
-        qk(sn, slot.k((st + 1) & 1));
+        // --- scores of step st+1 (MFMA) interleaved with the softmax of step
+        // st (VALU), then PV of step st (MFMA).  On the last step the scores
+        // are computed from a stale slot and discarded.
         Frag pf[NT][2];
+        if constexpr (sizeof(T) == 2) {
+            // An explicit software pipeline over the NF = NQ + NP MFMAs of the
+            // step: segment j issues MFMA j, the LDS read of the fragment that
+            // MFMA j + kReadLead consumes and a slice of the softmax, and
+            // sched_barrier keeps every segment in place, so each fragment
+            // arrives kReadLead MFMAs after its read was issued.  (Left to
+            // itself the scheduler, short of registers, reads each fragment
+            // right before its MFMA, which then waits out a whole LDS round
+            // trip.)  QK MFMAs alternate between the two 32-key tiles and PV
+            // MFMAs between the DT output tiles, so consecutive MFMAs never
+            // feed each other; every accumulator still sums in the same order.
+            constexpr int NQ = NT * KS, NP = NT * 2 * DT, NF = NQ + NP;
+            constexpr int EPS = NT * 16 / NQ;   // softmax elements per QK segment
+            static_assert(EPS * NQ == NT * 16, "softmax slices");
+            const T* kb = slot.k((st + 1) & 1);
+            const T* vb = slot.v(st & 1);
+            auto frag = [&](int j) -> Frag {
+                if (j < NQ)
+                    return load_frag<T>(kb + (32 * (j % NT) + lc) * C::KPAD + 16 * (j / NT) + 8 * h);
+                const int p = j - NQ, kt = p / (2 * DT), e = (p / DT) % 2, dt = p % DT;
+                return load_frag<T>(vb + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h);
+            };
+            Frag f[NF];
 #pragma unroll
-        for (int kt = 0; kt < NT; ++kt)
+            for (int kt = 0; kt < NT; ++kt) sn[kt] = zero16();
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
-        l_run += prob_sum<T, NT>(pf);
-        const T* vt_ = slot.v(st & 1);
+            for (int j = 0; j < kReadLead; ++j) f[j] = frag(j);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
+            for (int j = 0; j < NF; ++j) {
+                if (j < NQ) {
+                    mma(sn[j % NT], f[j], qf[j / NT]);
+                } else {
+                    const int p = j - NQ;
+                    mma(o[p % DT], f[j], pf[p / (2 * DT)][(p / DT) % 2]);
+                }
+                if (j + kReadLead < NF) f[j + kReadLead] = frag(j + kReadLead);
+                if (j < NQ) {
+#pragma unroll
+                    for (int u = 0; u < EPS; ++u) {
+                        const int x = j * EPS + u, kt = x / 16, r = x % 16;
+                        pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
+                    }
+                }
+                if (j == NQ) l_run += prob_sum<T, NT>(pf);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            qk(sn, slot.k((st + 1) & 1));
 #pragma unroll
             for (int kt = 0; kt < NT; ++kt)
 #pragma unroll
-                for (int e = 0; e < 2; ++e)
-                    mma(o[dt], load_frag<T>(vt_ + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h),
-                        pf[kt][e]);
-        if constexpr (sizeof(T) == 2) {
-            // LDS fragment reads run two ahead of the MFMAs that use them;
-            // 16 x (QK MFMA, read, 5 softmax VALU), then 16 x (PV MFMA, read,
-            // 2 VALU)
-            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                for (int r = 0; r < 16; ++r)
+                    pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
+            l_run += prob_sum<T, NT>(pf);
+            const T* vt_ = slot.v(st & 1);
 #pragma unroll
-            for (int g = 0; g < NT * KS; ++g) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x402, 5, 0);
-            }
+            for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int g = 0; g < DT * NT * 2; ++g) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x402, 2, 0);
-            }
+                for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+                    for (int e = 0; e < 2; ++e)
+                        mma(o[dt], load_frag<T>(vt_ + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h),
+                            pf[kt][e]);
         }
         // --- mask and max of step st+1
         if (st + 1 < steps && needs_mask(nb1))
