@@ -101,7 +101,7 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
                 t += (std::min(x * 128 + 127, s.np - 1) / 32) / kc + 1;
             return t * s.g;
         };
-        int kc = std::max(4, (ntiles + 3) / 4 * 4);
+        int kc = std::max(4, std::min((ntiles + 3) / 4 * 4, kEstMaxTiles));
         while (kc > 4 && groups(kc) < kFillGroups) kc = std::max(4, (kc / 2 + 3) / 4 * 4);
         s.est_kc = kc;
         s.est_nc = std::max(1, (ntiles + kc - 1) / kc);

@@ -339,19 +339,27 @@ __global__ __launch_bounds__(B * 2, 2) void mass_final_kernel(Shape sh, const T*
     const int blk0 = key0 / B, nblk = (key1 - key0 + B - 1) / B;
     const T* kbase = k + (int64_t)kvh * sh.kv_head;
 
-    // the row's normaliser from all chunks' partials, in chunk order
-    float L2 = 0.f;
+    // the row's normaliser from all chunks' partials: lane half h folds
+    // chunks h, h + 2, ... into a running (max, sum) in one pass, then the two
+    // halves (same row) combine
+    float mx = kNegInf, sx = 0.f;
     if (rl < nrows) {
-        const float* pp = part + ((int64_t)i * sh.nchunks * B + rl) * 2;
-        float mx = kNegInf;
-        for (int cc = 0; cc < sh.nchunks; ++cc) mx = fmaxf(mx, pp[(int64_t)cc * B * 2]);
-        float s = 0.f;
-        for (int cc = 0; cc < sh.nchunks; ++cc) {
-            const float mc = pp[(int64_t)cc * B * 2], lcc = pp[(int64_t)cc * B * 2 + 1];
-            if (mc != kNegInf) s += lcc * fast_exp2(mc - mx);
+        const float2* pp = reinterpret_cast<const float2*>(part) + (int64_t)i * sh.nchunks * B + rl;
+        for (int cc = h; cc < sh.nchunks; cc += 2) {
+            const float2 x = pp[(int64_t)cc * B];
+            if (x.x != kNegInf) {
+                const float mn = fmaxf(mx, x.x);
+                sx = (mx == kNegInf ? 0.f : sx * fast_exp2(mx - mn)) + x.y * fast_exp2(x.x - mn);
+                mx = mn;
+            }
         }
-        L2 = mx + log2f(s);
     }
+    const float mo = swap_halves(mx), so = swap_halves(sx);
+    const float mm = fmaxf(mx, mo);
+    // mm is finite for a valid row: key 0 (chunk 0) is visible to it
+    const float L2 = (rl < nrows) ? mm + log2f((mx == kNegInf ? 0.f : sx * fast_exp2(mx - mm)) +
+                                               (mo == kNegInf ? 0.f : so * fast_exp2(mo - mm)))
+                                  : 0.f;
     Frag qf[D / 16];
     {
         const T* qrow = q + (int64_t)min(t, n - 1) * sh.q_tok + (int64_t)i * sh.q_head;

@@ -52,6 +52,11 @@ constexpr int kMassChunk = 2048;
 // loops stop being split: 256 CUs x 2 resident workgroups x 2.
 constexpr int kFillGroups = 1024;
 
+// Longest key chunk of est_rowmax, in 32-key tiles: on long sequences every
+// workgroup is resident from the start, and without a cap the last row
+// band's chain of tiles (up to N'/32) would set the kernel's time.
+constexpr int kEstMaxTiles = 128;
+
 // Byte offsets of the workspace regions (each 256-byte aligned).
 struct WsLayout {
     size_t qg, kg;   // pooled proxy heads [G][N'][d] (problem dtype)

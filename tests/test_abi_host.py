@@ -101,8 +101,8 @@ def test_bad_struct_size_and_null_problem():
 def _key_chunks(n, hq, g, b, s):
     """The library's rule for splitting the estimation kernels' key loops:
     halve the mass kernels' 2048-key chunk (not below one block), and the
-    block-scoring chunk of 32-key tiles (a multiple of 4, not below 4), while
-    a launch has fewer than 1024 workgroups.  Returns (mass chunk, mass
+    block-scoring chunk of 32-key tiles (a multiple of 4, not below 4, at most
+    128), while a launch has fewer than 1024 workgroups.  Returns (mass chunk, mass
     chunks, tiles per scoring chunk, scoring chunks of the longest row)."""
     npr = -(-n // s)
     mc = 2048
@@ -113,16 +113,16 @@ def _key_chunks(n, hq, g, b, s):
     def groups(kc):
         return g * sum((min(x * 128 + 127, npr - 1) // 32) // kc + 1 for x in range(nrb))
 
-    kc = max(4, -(-nt // 4) * 4)
+    kc = max(4, min(-(-nt // 4) * 4, 128))
     while kc > 4 and groups(kc) < 1024:
         kc = max(4, -(-(kc // 2) // 4) * 4)
     return mc, -(-n // mc), kc, max(1, -(-nt // kc))
 
 
 def test_key_chunk_rule():
-    # long sequences keep one scoring chunk per row and 2048-key mass chunks
-    assert _key_chunks(131072, 32, 4, 128, 4) == (2048, 64, 1024, 1)
-    assert _key_chunks(262144, 32, 4, 128, 4) == (2048, 128, 2048, 1)
+    # long sequences: 2048-key mass chunks, scoring chunks of 128 tiles
+    assert _key_chunks(131072, 32, 4, 128, 4) == (2048, 64, 128, 8)
+    assert _key_chunks(262144, 32, 4, 128, 4) == (2048, 128, 128, 16)
     # short ones split until the launches reach 1024 workgroups (or the floor)
     assert _key_chunks(32768, 32, 4, 128, 4) == (1024, 32, 32, 8)
     assert _key_chunks(8192, 32, 4, 128, 4) == (256, 32, 4, 16)
