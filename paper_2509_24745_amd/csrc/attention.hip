@@ -123,6 +123,12 @@ struct AttnCfg {
     static constexpr int V_ELEMS = D * VPAD;
     static constexpr int STAGE = K_ELEMS + V_ELEMS;
     static constexpr int VPT = SUB / V / NTH;          // 16-byte vectors per thread per sub-block
+    // Waves per SIMD the LDS of one CU (160 KiB) leaves room for, capped at
+    // 2: the kernel's register budget.  d = 128 with b = 64 (two-wave
+    // workgroups), and fp32 at d = 128, are held to one wave per SIMD by LDS.
+    static constexpr int LDS_BYTES = 2 * STAGE * (int)sizeof(T) + 16;
+    static constexpr int WAVES_PER_SIMD_LDS = (160 * 1024 / LDS_BYTES) * (NTH / 64) / 4;
+    static constexpr int MIN_WAVES = WAVES_PER_SIMD_LDS < 1 ? 1 : (WAVES_PER_SIMD_LDS > 2 ? 2 : WAVES_PER_SIMD_LDS);
 };
 
 // Work item number `b` (b % 8 = queue, b / 8 = position in that queue).  The
@@ -580,7 +586,7 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
 // grid of one workgroup per item lets the engines that receive the long items
 // hold back all the others.
 template <typename T, int D, int B, bool DENSE>
-__global__ __launch_bounds__(2 * B, 2) void attn_kernel(Shape sh, const T* __restrict__ q,
+__global__ __launch_bounds__(2 * B, (AttnCfg<T, D, B>::MIN_WAVES)) void attn_kernel(Shape sh, const T* __restrict__ q,
                                                         const T* __restrict__ kvb,
                                                         const int* __restrict__ block_count,
                                                         const int* __restrict__ block_index,
