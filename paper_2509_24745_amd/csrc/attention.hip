@@ -281,6 +281,9 @@ __device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F7
 // MFMAs between the LDS read of an operand fragment and the MFMA that uses it
 // (bf16 attention loop).
 constexpr int kReadLead = 2;
+// First PV segment of the bf16 loop that folds the next step's scores into
+// the running row maxima.
+constexpr int kMaxSeg0 = 4;
 
 // Causal / ragged mask of one 64-key sub-tile: keys past `lim` (offset of
 // the last visible key inside the sub-tile) become -inf.  A key's offset is
@@ -477,6 +480,9 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
         // st (VALU), then PV of step st (MFMA).  On the last step the scores
         // are computed from a stale slot and discarded.
         Frag pf[NT][2];
+        // running maxima of step st+1's raw scores (four chains); the bf16
+        // pipeline folds them in during its PV segments
+        float c4[4] = {kNegInf, kNegInf, kNegInf, kNegInf};
         if constexpr (sizeof(T) == 2) {
             // An explicit software pipeline over the NF = NQ + NP MFMAs of the
             // step: segment j issues MFMA j, the LDS read of the fragment that
@@ -488,9 +494,16 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
             // trip.)  QK MFMAs alternate between the two 32-key tiles and PV
             // MFMAs between the DT output tiles, so consecutive MFMAs never
             // feed each other; every accumulator still sums in the same order.
+            // The probability sum and the next step's row maxima are VALU work
+            // for the PV segments; an empty asm that takes each result as an
+            // operand keeps it there (the optimizer would otherwise sink it to
+            // its use after the loop, where it runs behind the last MFMA).
             constexpr int NQ = NT * KS, NP = NT * 2 * DT, NF = NQ + NP;
             constexpr int EPS = NT * 16 / NQ;   // softmax elements per QK segment
             static_assert(EPS * NQ == NT * 16, "softmax slices");
+            static_assert(NP > kMaxSeg0, "PV segments for the row maxima");
+            // score pairs folded into the maxima per PV segment
+            constexpr int MPS = (NT * 8 + NP - kMaxSeg0 - 1) / (NP - kMaxSeg0);
             const T* kb = slot.k((st + 1) & 1);
             const T* vb = slot.v(st & 1);
             auto frag = [&](int j) -> Frag {
@@ -521,7 +534,23 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
                         pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
                     }
                 }
-                if (j == NQ) l_run += prob_sum<T, NT>(pf);
+                if (j == NQ) {
+                    l_run += prob_sum<T, NT>(pf);
+                    asm volatile("" : "+v"(l_run));
+                }
+                if (j >= NQ + kMaxSeg0) {
+                    // a tile's last QK MFMA was issued at least kMaxSeg0 + 1
+                    // segments earlier
+#pragma unroll
+                    for (int u = 0; u < MPS; ++u) {
+                        const int q2 = MPS * (j - NQ - kMaxSeg0) + u, kt = q2 / 8, r = 2 * (q2 % 8);
+                        if (q2 < NT * 8) {
+                            float& c = c4[(r >> 1) & 3];
+                            c = fmaxf(c, fmaxf(sn[kt][r], sn[kt][r + 1]));
+                            asm volatile("" : "+v"(c));
+                        }
+                    }
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         } else {
@@ -542,10 +571,16 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
                         mma(o[dt], load_frag<T>(vt_ + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h),
                             pf[kt][e]);
         }
-        // --- mask and max of step st+1
-        if (st + 1 < steps && needs_mask(nb1))
+        // --- mask and max of step st+1 (a masked sub-tile, rare, takes the
+        // maxima again after masking)
+        if (st + 1 < steps && needs_mask(nb1)) {
             mask_tail<NT>(sn, qlim - nb1 * B - ((st + 1) % C::NSUB) * C::KT, h);
-        mx = tile_max<NT>(sn) * sh.scale2;
+            mx = tile_max<NT>(sn) * sh.scale2;
+        } else if constexpr (sizeof(T) == 2) {
+            mx = halves_max(fmaxf(fmaxf(c4[0], c4[1]), fmaxf(c4[2], c4[3]))) * sh.scale2;
+        } else {
+            mx = tile_max<NT>(sn) * sh.scale2;
+        }
         nb0 = nb1;
         nb1 = nb2;
     };
