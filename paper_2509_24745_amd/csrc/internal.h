@@ -40,6 +40,10 @@ struct Shape {
 // Number of XCDs workgroups are dealt to round-robin on MI355X.
 constexpr int kNumXcd = 8;
 
+// MI355X's last-level memory-side cache (Infinity Cache / MALL), shared by all
+// XCDs.
+constexpr size_t kMallBytes = (size_t)256 << 20;
+
 // The attention kernel is persistent: its workgroups pull work items from
 // kNumXcd queues (one int32 counter per queue, each on its own 128-byte line).
 constexpr int kQueueStride = 32;

@@ -261,6 +261,42 @@ def test_deterministic_across_runs_and_streams():
             assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("wl", [LLAMA.replace(seq_len=4096 + 77), QWEN.replace(seq_len=3000)],
+                         ids=["llama_n4173", "qwen_n3000"])
+def test_work_orders_give_identical_output(wl, monkeypatch):
+    """Every work order and chunk size must hand each (head, block row) item to
+    exactly one workgroup, which computes it alone: sparse and dense outputs
+    and lse are then bitwise those of the default order (ragged N, GQA 4 and
+    7, chunk sizes that do not divide the block rows)."""
+    U = _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    qd, kd, vd = U.to_dev(q, prob), U.to_dev(k, prob), U.to_dev(v, prob)
+    b = pa.prefill(prob, qd, kd, vd, wl.gamma)
+    torch.cuda.synchronize()
+
+    def run(dense):
+        out = torch.full_like(b.out, float("nan"))
+        lse = torch.full_like(b.lse, float("nan"))
+        if dense:
+            pa.proxyattn_dense_prefill(prob, qd, kd, vd, out, lse, b.workspace)
+        else:
+            pa.proxyattn_block_sparse_prefill(prob, qd, kd, vd, b.block_count, b.block_index,
+                                              out, lse, b.workspace)
+        torch.cuda.synchronize()
+        return out.cpu(), lse.cpu()
+
+    ref = {dense: run(dense) for dense in (False, True)}
+    for order, rows in ((0, 1), (1, 1), (1, 3), (2, 1), (2, 4), (2, 7)):
+        monkeypatch.setenv("PROXYATTN_ATTN_ORDER", str(order))
+        monkeypatch.setenv("PROXYATTN_ATTN_CHUNK_ROWS", str(rows))
+        for dense in (False, True):
+            out, lse = run(dense)
+            assert torch.equal(out, ref[dense][0]), (order, rows, dense)
+            assert torch.equal(lse, ref[dense][1]), (order, rows, dense)
+
+
 def test_empty_problem_is_a_noop():
     _gpu()
     from paper_2509_24745_amd import proxyattn as pa
