@@ -24,10 +24,10 @@
 // G * Mq(Mq+1)/2 * b' * 4 bytes of workspace.
 //
 // Last-block mass (a4): the last min(b, N) query tokens of every head
-// against all keys, split into key chunks for parallelism.
-//   mass_partial: per (head, chunk) the rows' partial (max, sum).
-//   mass_final:   combines the partials into each row's normaliser, recomputes
-//     the tiles and sums exp(S - L) per key block over keys and rows.
+// against all keys, split into key chunks for parallelism, in one pass.
+//   mass_block:  per (head, row, key block) the block's (max, sum of exp2).
+//   mass_reduce: each row's normaliser from its blocks, then per key block
+//     the sum over rows of the block's share.
 #include "common.h"
 #include "internal.h"
 
@@ -244,12 +244,19 @@ __global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* 
 }
 
 // ---------------------------------------------------------------------------
-// a4: last-block mass.  grid (nchunks, Hq), B*2 threads (B/32 waves).
+// a4: last-block mass, one pass over the keys.
+// mass_block: grid (nchunks, Hq), B*2 threads (B/32 waves, 32 last-block rows
+//   each).  For every (row, key block) of its key chunk: the block's largest
+//   scaled logit m and the sum of exp2(logit - m) over the block's visible
+//   keys, written to part[i][row][block] (float2).
+// mass_reduce: grid (Hq), 1024 threads.  Each row's log2-sum-exp over its
+//   visible blocks, then mass[i][n] = sum over rows of s * exp2(m - L) (rows
+//   in order: a fixed-order sum).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int B>
-__global__ __launch_bounds__(B * 2, 2) void mass_partial_kernel(Shape sh, const T* __restrict__ q,
-                                                             const T* __restrict__ k,
-                                                             float* __restrict__ part) {
+__global__ __launch_bounds__(B * 2, 2) void mass_block_kernel(Shape sh, const T* __restrict__ q,
+                                                          const T* __restrict__ k,
+                                                          float2* __restrict__ part) {
     typedef typename FragOf<T>::type Frag;
     constexpr int NTH = B * 2;
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, NTH>::LDT];
@@ -271,7 +278,8 @@ __global__ __launch_bounds__(B * 2, 2) void mass_partial_kernel(Shape sh, const 
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
     }
-    float m = kNegInf, l = 0.f;
+    // this lane's running (max, sum of exp2) over its keys of the current block
+    float bm = kNegInf, bs = 0.f;
     KeyTile<T, D, NTH> ld;
     ld.load(kbase, sh.kv_tok, kt0 * 32, n, tid);
     ld.store(tiles[0], tid);
@@ -292,118 +300,85 @@ __global__ __launch_bounds__(B * 2, 2) void mass_partial_kernel(Shape sh, const 
             for (int j = 0; j < 4; ++j)
                 c4[j] = fmaxf(fmaxf(acc[4 * j], acc[4 * j + 1]), fmaxf(acc[4 * j + 2], acc[4 * j + 3]));
             const float tm = fmaxf(fmaxf(c4[0], c4[1]), fmaxf(c4[2], c4[3])) * sh.scale2;
-            const float mn = fmaxf(m, tm);
+            const float mn = fmaxf(bm, tm);
             if (mn != kNegInf) {
                 const float neg = -mn;
                 float sp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int r = 0; r < 16; ++r) sp[r & 3] += fast_exp2(fmaf(acc[r], sh.scale2, neg));
-                l = fmaf(l, fast_exp2(m - mn), (sp[0] + sp[1]) + (sp[2] + sp[3]));
-                m = mn;
+                bs = fmaf(bs, bm == kNegInf ? 0.f : fast_exp2(bm - mn), (sp[0] + sp[1]) + (sp[2] + sp[3]));
+                bm = mn;
             }
+        }
+        if (((kt + 1) * 32) % B == 0 || kt == kt1) {
+            // block done: combine the two lane halves (one row) and store
+            const float mo = swap_halves(bm), so = swap_halves(bs);
+            const float mm = fmaxf(bm, mo);
+            const float ss = (bm == kNegInf ? 0.f : bs * fast_exp2(bm - mm)) +
+                             (mo == kNegInf ? 0.f : so * fast_exp2(mo - mm));
+            if (wave_on && h == 0 && rl < nrows)
+                part[((int64_t)i * B + rl) * sh.mq + (kt * 32) / B] = make_float2(mm, ss);
+            bm = kNegInf;
+            bs = 0.f;
         }
         if (kt < kt1) ld.store(tiles[buf ^ 1], tid);
         __syncthreads();
-    }
-    const float mo = swap_halves(m), lo = swap_halves(l);
-    const float mm = fmaxf(m, mo);
-    if (h == 0 && rl < nrows) {
-        const float ll = (mm == kNegInf) ? 0.f : l * fast_exp2(m - mm) + lo * fast_exp2(mo - mm);
-        float* pp = part + (((int64_t)i * sh.nchunks + c) * B + rl) * 2;
-        pp[0] = mm;
-        pp[1] = ll;
     }
 }
 
-template <typename T, int D, int B>
-__global__ __launch_bounds__(B * 2, 2) void mass_final_kernel(Shape sh, const T* __restrict__ q,
-                                                           const T* __restrict__ k,
-                                                           const float* __restrict__ part,
-                                                           float* __restrict__ mass) {
-    typedef typename FragOf<T>::type Frag;
-    constexpr int NTH = B * 2, NW = B / 32;
-    constexpr int BPC = kMassChunk / B;  // blocks per chunk, at most
-    __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, NTH>::LDT];
-    __shared__ float wpart[NW][BPC];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
-    const int c = blockIdx.x, i = blockIdx.y, kvh = i / sh.rep;
-    const int n = sh.n;
-    const int nrows = min(B, n), t0 = n - nrows;
-    const int rl = 32 * w + lc, t = t0 + rl;
-    const bool wave_on = 32 * w < nrows;
-    const int wave_first_t = t0 + 32 * w;
-    const int wave_last_t = t0 + min(32 * w + 31, nrows - 1);
-    const bool wave_full = 32 * w + 31 < nrows;
-    const int key0 = c * sh.mass_chunk, key1 = min(key0 + sh.mass_chunk, n);
-    const int kt0 = key0 / 32, kt1 = (key1 - 1) / 32;
-    const int blk0 = key0 / B, nblk = (key1 - key0 + B - 1) / B;
-    const T* kbase = k + (int64_t)kvh * sh.kv_head;
+constexpr int kMassReduceThreads = 1024;
 
-    // the row's normaliser from all chunks' partials: lane half h folds
-    // chunks h, h + 2, ... into a running (max, sum) in one pass, then the two
-    // halves (same row) combine
-    float mx = kNegInf, sx = 0.f;
-    if (rl < nrows) {
-        const float2* pp = reinterpret_cast<const float2*>(part) + (int64_t)i * sh.nchunks * B + rl;
-        for (int cc = h; cc < sh.nchunks; cc += 2) {
-            const float2 x = pp[(int64_t)cc * B];
+__global__ __launch_bounds__(kMassReduceThreads) void mass_reduce_kernel(Shape sh,
+                                                                        const float2* __restrict__ part,
+                                                                        float* __restrict__ mass) {
+    __shared__ float L[128];
+    constexpr int NW = kMassReduceThreads / 64;
+    const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int b = sh.b, mq = sh.mq;
+    const int nrows = min(b, sh.n), t0 = sh.n - nrows;
+    const float2* base = part + (int64_t)i * b * mq;
+    // each row's normaliser over its visible blocks n <= t / b (block n holds
+    // key n b <= t, so every one of them was written)
+    for (int r = w; r < nrows; r += NW) {
+        const int nmax = (t0 + r) / b;
+        const float2* pr = base + (int64_t)r * mq;
+        float m = kNegInf, s = 0.f;
+        for (int nb = lane; nb <= nmax; nb += 64) {
+            const float2 x = pr[nb];
             if (x.x != kNegInf) {
-                const float mn = fmaxf(mx, x.x);
-                sx = (mx == kNegInf ? 0.f : sx * fast_exp2(mx - mn)) + x.y * fast_exp2(x.x - mn);
-                mx = mn;
+                const float mn = fmaxf(m, x.x);
+                s = (m == kNegInf ? 0.f : s * fast_exp2(m - mn)) + x.y * fast_exp2(x.x - mn);
+                m = mn;
             }
         }
+        const float M = wave_max(m);   // finite: block 0 is visible to every row
+        const float sv = wave_sum(m == kNegInf ? 0.f : s * fast_exp2(m - M));
+        if (lane == 0) L[r] = M + log2f(sv);
     }
-    const float mo = swap_halves(mx), so = swap_halves(sx);
-    const float mm = fmaxf(mx, mo);
-    // mm is finite for a valid row: key 0 (chunk 0) is visible to it
-    const float L2 = (rl < nrows) ? mm + log2f((mx == kNegInf ? 0.f : sx * fast_exp2(mx - mm)) +
-                                               (mo == kNegInf ? 0.f : so * fast_exp2(mo - mm)))
-                                  : 0.f;
-    Frag qf[D / 16];
-    {
-        const T* qrow = q + (int64_t)min(t, n - 1) * sh.q_tok + (int64_t)i * sh.q_head;
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
-    }
-    KeyTile<T, D, NTH> ld;
-    ld.load(kbase, sh.kv_tok, kt0 * 32, n, tid);
-    ld.store(tiles[0], tid);
     __syncthreads();
-    float acc_blk = 0.f;
-    for (int kt = kt0; kt <= kt1; ++kt) {
-        const int buf = (kt - kt0) & 1;
-        if (kt < kt1) ld.load(kbase, sh.kv_tok, (kt + 1) * 32, n, tid);
-        if (wave_on && kt * 32 <= wave_last_t) {
-            const f32x16 acc = st_tile<T, D>(tiles[buf], qf, lc, h);
-            const float neg = -L2;
-            float sp[4] = {0.f, 0.f, 0.f, 0.f};
-            if (wave_full && kt * 32 + 31 <= wave_first_t) {
-                // every key of the tile is visible to every row of the wave
-#pragma unroll
-                for (int r = 0; r < 16; ++r) sp[r & 3] += fast_exp2(fmaf(acc[r], sh.scale2, neg));
-            } else {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int u = kt * 32 + c_row(r, h);
-                    sp[r & 3] += (u <= t && rl < nrows) ? fast_exp2(fmaf(acc[r], sh.scale2, neg)) : 0.f;
+    // 64 blocks at a time, one per lane; wave w sums rows w, w + NW, ... and
+    // wave 0 adds the NW partial sums in order
+    __shared__ float ps[NW][64];
+    for (int nb0 = 0; nb0 < mq; nb0 += 64) {
+        const int nb = nb0 + lane;
+        float acc = 0.f;
+        if (nb < mq) {
+            for (int r = w; r < nrows; r += NW) {
+                if (nb * b <= t0 + r) {
+                    const float2 x = base[(int64_t)r * mq + nb];
+                    if (x.x != kNegInf) acc += x.y * fast_exp2(x.x - L[r]);
                 }
             }
-            acc_blk += (sp[0] + sp[1]) + (sp[2] + sp[3]);
         }
-        if (((kt + 1) * 32) % B == 0 || kt == kt1) {
-            const float s = wave_sum(acc_blk);
-            if (lane == 0) wpart[w][(kt * 32) / B - blk0] = s;
-            acc_blk = 0.f;
-        }
-        if (kt < kt1) ld.store(tiles[buf ^ 1], tid);
+        ps[w][lane] = acc;
         __syncthreads();
-    }
-    for (int bl = tid; bl < nblk; bl += NTH) {
-        float s = 0.f;
+        if (w == 0 && nb < mq) {
+            float sum = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) s += wpart[ww][bl];
-        mass[(int64_t)i * sh.mq + blk0 + bl] = s;
+            for (int ww = 0; ww < NW; ++ww) sum += ps[ww][lane];
+            mass[(int64_t)i * mq + nb] = sum;
+        }
+        __syncthreads();
     }
 }
 
@@ -447,19 +422,18 @@ hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* ro
 }
 
 template <typename T, int D, int B>
-static hipError_t mass_t(const Shape& sh, const void* q, const void* k, float* part, float* mass,
+static hipError_t mass_t(const Shape& sh, const void* q, const void* k, float2* part, float* mass,
                          hipStream_t st) {
-    dim3 grid(sh.nchunks, sh.hq);
-    hipLaunchKernelGGL((mass_partial_kernel<T, D, B>), grid, dim3(B * 2), 0, st, sh, (const T*)q,
-                       (const T*)k, part);
+    hipLaunchKernelGGL((mass_block_kernel<T, D, B>), dim3(sh.nchunks, sh.hq), dim3(B * 2), 0, st, sh,
+                       (const T*)q, (const T*)k, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((mass_final_kernel<T, D, B>), grid, dim3(B * 2), 0, st, sh, (const T*)q,
-                       (const T*)k, (const float*)part, mass);
+    hipLaunchKernelGGL(mass_reduce_kernel, dim3(sh.hq), dim3(kMassReduceThreads), 0, st, sh,
+                       (const float2*)part, mass);
     return hipGetLastError();
 }
 
-hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float* part, float* mass,
+hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* mass,
                        hipStream_t st) {
     if (sh.dtype == 0) {
         if (sh.d == 64) return sh.b == 64 ? mass_t<bf16, 64, 64>(sh, q, k, part, mass, st)

@@ -138,9 +138,9 @@ def test_workspace_size_formula(n, hq, hkv, g, b, s):
     prob = _prob(seq_len=n, num_q_heads=hq, num_kv_heads=hkv, num_proxy_groups=g,
                  block_size=b, stride=s)
     npr, mq, bp = -(-n // s), -(-n // b), b // s
-    _, nchunks, _, est_nc = _key_chunks(n, hq, g, b, s)
+    _, _, _, est_nc = _key_chunks(n, hq, g, b, s)
     regions = [g * npr * d * 2, g * npr * d * 2, g * est_nc * npr * 8,
-               g * (mq * (mq + 1) // 2) * bp * 4, hq * nchunks * b * 2 * 4,
+               g * (mq * (mq + 1) // 2) * bp * 4, hq * b * mq * 8,
                hkv * mq * 2 * d * b * 2, 8 * 32 * 4]
     end = sum(-(-r // 256) * 256 for r in regions)
     kvb = sum(-(-r // 256) * 256 for r in regions[:5])
