@@ -145,6 +145,7 @@ WsLayout ws_layout(const Shape& sh) {
     L.rowpart = off; off = align_up(off + (size_t)sh.g * sh.est_nc * sh.np * 8);
     L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.b * sh.mq * 8);
+    L.lnorm = off; off = align_up(off + (size_t)sh.hq * sh.b * 4);
     L.kvb = off;  off = align_up(off + (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz);
     L.queue = off; off = align_up(off + (size_t)kNumXcd * kQueueStride * 4);
     // the diagnostic reuses the re-blocked K/V region (never live at the same time)
@@ -227,7 +228,8 @@ int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
                                 (float2*)(ws + L.rowpart), st), "est_rowmax");
     PA_LAUNCH(launch_est_reduce(sh, (const float*)(ws + L.rbm), (const float2*)(ws + L.rowpart),
                                 block_logscore, st), "est_reduce");
-    PA_LAUNCH(launch_mass(sh, q, k, (float2*)(ws + L.part), lastblk_mass, st), "mass");
+    PA_LAUNCH(launch_mass(sh, q, k, (float2*)(ws + L.part), (float*)(ws + L.lnorm), lastblk_mass, st),
+              "mass");
     return PROXYATTN_OK;
 }
 

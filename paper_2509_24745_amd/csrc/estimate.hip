@@ -26,8 +26,8 @@
 // Last-block mass (a4): the last min(b, N) query tokens of every head
 // against all keys, split into key chunks for parallelism, in one pass.
 //   mass_block:  per (head, row, key block) the block's (max, sum of exp2).
-//   mass_reduce: each row's normaliser from its blocks, then per key block
-//     the sum over rows of the block's share.
+//   mass_norm:   each row's normaliser from its blocks.
+//   mass_sum:    per key block, the sum over rows of the block's share.
 #include "common.h"
 #include "internal.h"
 
@@ -249,9 +249,8 @@ __global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* 
 //   each).  For every (row, key block) of its key chunk: the block's largest
 //   scaled logit m and the sum of exp2(logit - m) over the block's visible
 //   keys, written to part[i][row][block] (float2).
-// mass_reduce: grid (Hq), 1024 threads.  Each row's log2-sum-exp over its
-//   visible blocks, then mass[i][n] = sum over rows of s * exp2(m - L) (rows
-//   in order: a fixed-order sum).
+// mass_norm, mass_sum: each row's log2-sum-exp over its visible blocks, then
+//   mass[i][n] = sum over rows of s * exp2(m - L) in a fixed order.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int B>
 __global__ __launch_bounds__(B * 2, 2) void mass_block_kernel(Shape sh, const T* __restrict__ q,
@@ -326,59 +325,69 @@ __global__ __launch_bounds__(B * 2, 2) void mass_block_kernel(Shape sh, const T*
     }
 }
 
-constexpr int kMassReduceThreads = 1024;
+constexpr int kMassReduceThreads = 1024;   // 16 waves
 
-__global__ __launch_bounds__(kMassReduceThreads) void mass_reduce_kernel(Shape sh,
-                                                                        const float2* __restrict__ part,
-                                                                        float* __restrict__ mass) {
-    __shared__ float L[128];
+// Row normalisers: grid (Hq, ceil(rows / 16)), one wave per last-block row:
+// the row's log2-sum-exp over its visible blocks n <= t / b (block n holds
+// key n b <= t, so every one of them was written).
+__global__ __launch_bounds__(kMassReduceThreads) void mass_norm_kernel(Shape sh,
+                                                                      const float2* __restrict__ part,
+                                                                      float* __restrict__ lnorm) {
     constexpr int NW = kMassReduceThreads / 64;
+    const int i = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int b = sh.b, mq = sh.mq;
+    const int nrows = min(b, sh.n), t0 = sh.n - nrows;
+    const int r = blockIdx.y * NW + w;
+    if (r >= nrows) return;   // whole waves; no barrier follows
+    const int nmax = (t0 + r) / b;
+    const float2* pr = part + ((int64_t)i * b + r) * mq;
+    float m = kNegInf, s = 0.f;
+    for (int nb = lane; nb <= nmax; nb += 64) {
+        const float2 x = pr[nb];
+        if (x.x != kNegInf) {
+            const float mn = fmaxf(m, x.x);
+            s = (m == kNegInf ? 0.f : s * fast_exp2(m - mn)) + x.y * fast_exp2(x.x - mn);
+            m = mn;
+        }
+    }
+    const float M = wave_max(m);   // finite: block 0 is visible to every row
+    const float sv = wave_sum(m == kNegInf ? 0.f : s * fast_exp2(m - M));
+    if (lane == 0) lnorm[(int64_t)i * b + r] = M + log2f(sv);
+}
+
+// Block masses: grid (Hq, ceil(Nk / 64)), 64 blocks per workgroup, one per
+// lane; wave w sums rows w, w + 16, ... and wave 0 adds the 16 partial sums in
+// order (a fixed-order sum).
+__global__ __launch_bounds__(kMassReduceThreads) void mass_sum_kernel(Shape sh,
+                                                                     const float2* __restrict__ part,
+                                                                     const float* __restrict__ lnorm,
+                                                                     float* __restrict__ mass) {
+    constexpr int NW = kMassReduceThreads / 64;
+    __shared__ float L[128];
+    __shared__ float ps[NW][64];
     const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int b = sh.b, mq = sh.mq;
     const int nrows = min(b, sh.n), t0 = sh.n - nrows;
-    const float2* base = part + (int64_t)i * b * mq;
-    // each row's normaliser over its visible blocks n <= t / b (block n holds
-    // key n b <= t, so every one of them was written)
-    for (int r = w; r < nrows; r += NW) {
-        const int nmax = (t0 + r) / b;
-        const float2* pr = base + (int64_t)r * mq;
-        float m = kNegInf, s = 0.f;
-        for (int nb = lane; nb <= nmax; nb += 64) {
-            const float2 x = pr[nb];
-            if (x.x != kNegInf) {
-                const float mn = fmaxf(m, x.x);
-                s = (m == kNegInf ? 0.f : s * fast_exp2(m - mn)) + x.y * fast_exp2(x.x - mn);
-                m = mn;
-            }
-        }
-        const float M = wave_max(m);   // finite: block 0 is visible to every row
-        const float sv = wave_sum(m == kNegInf ? 0.f : s * fast_exp2(m - M));
-        if (lane == 0) L[r] = M + log2f(sv);
-    }
+    for (int r = tid; r < nrows; r += kMassReduceThreads) L[r] = lnorm[(int64_t)i * b + r];
     __syncthreads();
-    // 64 blocks at a time, one per lane; wave w sums rows w, w + NW, ... and
-    // wave 0 adds the NW partial sums in order
-    __shared__ float ps[NW][64];
-    for (int nb0 = 0; nb0 < mq; nb0 += 64) {
-        const int nb = nb0 + lane;
-        float acc = 0.f;
-        if (nb < mq) {
-            for (int r = w; r < nrows; r += NW) {
-                if (nb * b <= t0 + r) {
-                    const float2 x = base[(int64_t)r * mq + nb];
-                    if (x.x != kNegInf) acc += x.y * fast_exp2(x.x - L[r]);
-                }
+    const float2* base = part + (int64_t)i * b * mq;
+    const int nb = blockIdx.y * 64 + lane;
+    float acc = 0.f;
+    if (nb < mq) {
+        for (int r = w; r < nrows; r += NW) {
+            if (nb * b <= t0 + r) {
+                const float2 x = base[(int64_t)r * mq + nb];
+                if (x.x != kNegInf) acc += x.y * fast_exp2(x.x - L[r]);
             }
         }
-        ps[w][lane] = acc;
-        __syncthreads();
-        if (w == 0 && nb < mq) {
-            float sum = 0.f;
+    }
+    ps[w][lane] = acc;
+    __syncthreads();
+    if (w == 0 && nb < mq) {
+        float sum = 0.f;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) sum += ps[ww][lane];
-            mass[(int64_t)i * mq + nb] = sum;
-        }
-        __syncthreads();
+        for (int ww = 0; ww < NW; ++ww) sum += ps[ww][lane];
+        mass[(int64_t)i * mq + nb] = sum;
     }
 }
 
@@ -422,29 +431,34 @@ hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* ro
 }
 
 template <typename T, int D, int B>
-static hipError_t mass_t(const Shape& sh, const void* q, const void* k, float2* part, float* mass,
-                         hipStream_t st) {
+static hipError_t mass_t(const Shape& sh, const void* q, const void* k, float2* part, float* lnorm,
+                         float* mass, hipStream_t st) {
     hipLaunchKernelGGL((mass_block_kernel<T, D, B>), dim3(sh.nchunks, sh.hq), dim3(B * 2), 0, st, sh,
                        (const T*)q, (const T*)k, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(mass_reduce_kernel, dim3(sh.hq), dim3(kMassReduceThreads), 0, st, sh,
-                       (const float2*)part, mass);
+    constexpr int NW = kMassReduceThreads / 64;
+    hipLaunchKernelGGL(mass_norm_kernel, dim3(sh.hq, (min(sh.b, sh.n) + NW - 1) / NW),
+                       dim3(kMassReduceThreads), 0, st, sh, (const float2*)part, lnorm);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(mass_sum_kernel, dim3(sh.hq, (sh.mq + 63) / 64), dim3(kMassReduceThreads), 0,
+                       st, sh, (const float2*)part, (const float*)lnorm, mass);
     return hipGetLastError();
 }
 
-hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* mass,
-                       hipStream_t st) {
+hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* lnorm,
+                       float* mass, hipStream_t st) {
     if (sh.dtype == 0) {
-        if (sh.d == 64) return sh.b == 64 ? mass_t<bf16, 64, 64>(sh, q, k, part, mass, st)
-                                          : mass_t<bf16, 64, 128>(sh, q, k, part, mass, st);
-        return sh.b == 64 ? mass_t<bf16, 128, 64>(sh, q, k, part, mass, st)
-                          : mass_t<bf16, 128, 128>(sh, q, k, part, mass, st);
+        if (sh.d == 64) return sh.b == 64 ? mass_t<bf16, 64, 64>(sh, q, k, part, lnorm, mass, st)
+                                          : mass_t<bf16, 64, 128>(sh, q, k, part, lnorm, mass, st);
+        return sh.b == 64 ? mass_t<bf16, 128, 64>(sh, q, k, part, lnorm, mass, st)
+                          : mass_t<bf16, 128, 128>(sh, q, k, part, lnorm, mass, st);
     }
-    if (sh.d == 64) return sh.b == 64 ? mass_t<float, 64, 64>(sh, q, k, part, mass, st)
-                                      : mass_t<float, 64, 128>(sh, q, k, part, mass, st);
-    return sh.b == 64 ? mass_t<float, 128, 64>(sh, q, k, part, mass, st)
-                      : mass_t<float, 128, 128>(sh, q, k, part, mass, st);
+    if (sh.d == 64) return sh.b == 64 ? mass_t<float, 64, 64>(sh, q, k, part, lnorm, mass, st)
+                                      : mass_t<float, 64, 128>(sh, q, k, part, lnorm, mass, st);
+    return sh.b == 64 ? mass_t<float, 128, 64>(sh, q, k, part, lnorm, mass, st)
+                      : mass_t<float, 128, 128>(sh, q, k, part, lnorm, mass, st);
 }
 
 }  // namespace pa

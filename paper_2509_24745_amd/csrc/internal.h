@@ -68,6 +68,7 @@ struct WsLayout {
     size_t rbm;      // per-(row, key block) max of the scaled proxy logits,
                      // [G][Mq(Mq+1)/2][b'] fp32 (lower-triangular block pairs)
     size_t part;     // last-block (max, sum) per (head, row, key block) [Hq][b][Mq] float2
+    size_t lnorm;    // last-block rows' log2-sum-exp [Hq][b] fp32
     size_t kvb;      // re-blocked K and V^T [Hkv][Mq][2 b d] (problem dtype)
     size_t queue;    // attention work-queue counters [kNumXcd][kQueueStride] int32
     size_t diag;     // head-overlap diagnostic: probabilities [Hq][N] fp32, then the
@@ -83,8 +84,8 @@ hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, fl
                              float2* rowpart, hipStream_t st);
 hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* rowpart,
                              float* logA, hipStream_t st);
-hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* mass,
-                       hipStream_t st);
+hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* lnorm,
+                       float* mass, hipStream_t st);
 hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,

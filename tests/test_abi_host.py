@@ -140,10 +140,10 @@ def test_workspace_size_formula(n, hq, hkv, g, b, s):
     npr, mq, bp = -(-n // s), -(-n // b), b // s
     _, _, _, est_nc = _key_chunks(n, hq, g, b, s)
     regions = [g * npr * d * 2, g * npr * d * 2, g * est_nc * npr * 8,
-               g * (mq * (mq + 1) // 2) * bp * 4, hq * b * mq * 8,
+               g * (mq * (mq + 1) // 2) * bp * 4, hq * b * mq * 8, hq * b * 4,
                hkv * mq * 2 * d * b * 2, 8 * 32 * 4]
     end = sum(-(-r // 256) * 256 for r in regions)
-    kvb = sum(-(-r // 256) * 256 for r in regions[:5])
+    kvb = sum(-(-r // 256) * 256 for r in regions[:6])
     diag_end = kvb + -(-(hq * n * 4) // 256) * 256 + -(-(hq * 8) // 256) * 256
     assert pa.proxyattn_workspace_size(prob) == max(end, diag_end)
 
