@@ -133,6 +133,41 @@ def test_pipeline_matches_oracle(case):
     _compare(wl, q, k, v, gpu, orc)
 
 
+def _random_workload(seed: int) -> Workload:
+    """A seeded draw from the supported shapes: dtype, d, b, stride, GQA
+    ratio, proxy groups (a divisor of Hq), N from 1 to 2600 (partial and
+    single blocks included), gamma, minimum budget and input structure."""
+    rng = np.random.default_rng(1000 + seed)
+    dtype = "fp32" if rng.random() < 0.25 else "bf16"
+    d = int(rng.choice([64, 128]))
+    b = int(rng.choice([64, 128]))
+    stride = int(rng.choice([1, 2, 4]))
+    hkv = int(rng.choice([1, 2, 3, 4]))
+    rep = int(rng.choice([r for r in (1, 2, 3, 4, 7) if hkv * r <= 16]))
+    hq = hkv * rep
+    groups = int(rng.choice([g for g in range(1, hq + 1) if hq % g == 0]))
+    n = int(rng.integers(1, 2601))
+    return Workload(name=f"rand{seed}", seq_len=n, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                    block_size=b, num_proxy_groups=groups, stride=stride, dtype=dtype,
+                    gamma=float(rng.uniform(0.8, 0.99)),
+                    min_budget_tokens=int(rng.choice([0, 0, 2 * b])),
+                    structure=Structure(rank=int(rng.choice([4, 8, 16])),
+                                        noise=float(rng.uniform(0.1, 0.6)),
+                                        hetero=bool(rng.random() < 0.3)), seed=seed)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_shapes_match_oracle(seed):
+    U = _gpu()
+    wl = _random_workload(seed)
+    print(f"\n[random {seed}] {wl}", flush=True)
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    gpu = U.run_path(prob, q, k, v, wl.gamma, wl.min_budget_tokens)
+    orc = _oracle(wl, q, k)
+    _compare(wl, q, k, v, gpu, orc)
+
+
 def test_min_budget_and_full_budget():
     U = _gpu()
     wl = LLAMA.replace(seq_len=4096, min_budget_tokens=2048)
