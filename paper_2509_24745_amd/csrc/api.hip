@@ -83,10 +83,10 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     s.bp = p->block_size / p->stride;
     s.rep = p->num_q_heads / p->num_kv_heads;
     s.gsize = p->num_q_heads / p->num_proxy_groups;
-    // Key loops of the estimation kernels: one chunk per row (or per 2048
-    // keys) on long sequences; split further while a launch would have fewer
-    // than kFillGroups workgroups, so that short sequences do not leave most
-    // CUs idle behind a few long chains.
+    // Key loops of the estimation kernels: chunks of at most kMassChunk keys
+    // (mass) and kEstMaxTiles 32-key tiles (block scoring), split further
+    // while a launch would have fewer than kFillGroups workgroups, so that
+    // short sequences do not leave most CUs idle behind a few long chains.
     {
         int mc = kMassChunk;
         while (mc > s.b && (int64_t)s.hq * ((s.n + mc - 1) / mc) < kFillGroups) mc /= 2;

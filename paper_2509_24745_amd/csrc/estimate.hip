@@ -17,8 +17,9 @@
 //     log2-sum-exp L2[t'], then logA[m, n] = ln2 * max_{t' in m}
 //     (rbm[m, n][t'] - L2[t']) = log max_{t', u'} softmax(...)  (the
 //     max-pool of Eq. 1, log domain).
-// Long sequences use one chunk per row (the whole causal key range); short
-// ones split it so that the launch still fills the chip.
+// A row's key range is cut into chunks of at most kEstMaxTiles 32-key tiles
+// (so that no workgroup's chain of tiles sets the kernel's time), and further
+// on short sequences so that the launch still fills the chip.
 // One MFMA pass instead of two (no recomputation of the tiles to re-derive
 // the max-pool after the row normaliser is known); rbm costs
 // G * Mq(Mq+1)/2 * b' * 4 bytes of workspace.
