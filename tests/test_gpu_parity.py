@@ -79,13 +79,13 @@ CASES = {
 }
 
 
-def _oracle(wl, q, k, v=None):
+def _oracle(wl, q, k, v=None, scale=None):
     return O.proxyattn_prefill(q, k, v, num_groups=wl.num_proxy_groups, block_size=wl.block_size,
                                stride=wl.stride, gamma=wl.gamma,
-                               min_budget_tokens=wl.min_budget_tokens, dtype=wl.dtype)
+                               min_budget_tokens=wl.min_budget_tokens, scale=scale, dtype=wl.dtype)
 
 
-def _compare(wl, q, k, v, gpu, orc, attn_rows=None):
+def _compare(wl, q, k, v, gpu, orc, attn_rows=None, scale=None):
     rep = C.Report()
     # pooled heads: bit-exact
     assert np.array_equal(gpu["qg"], orc["qg"]), "pooled queries differ"
@@ -108,9 +108,9 @@ def _compare(wl, q, k, v, gpu, orc, attn_rows=None):
                   report=rep)
     # attention on the GPU's lists
     if v is not None:
+        sc = O.default_scale(wl.head_dim) if scale is None else scale
         ref_out, ref_lse = O.block_sparse_attention(q, k, v, gpu["block_count"], gpu["block_index"],
-                                                    wl.block_size, O.default_scale(wl.head_dim),
-                                                    query_rows=attn_rows)
+                                                    wl.block_size, sc, query_rows=attn_rows)
         sel = slice(None) if attn_rows is None else np.asarray(attn_rows)
         C.check_attention(gpu["out"][sel], ref_out[sel], rep)
         dl = np.abs(gpu["lse"][:, sel] - ref_lse[:, sel])
@@ -166,6 +166,19 @@ def test_random_shapes_match_oracle(seed):
     gpu = U.run_path(prob, q, k, v, wl.gamma, wl.min_budget_tokens)
     orc = _oracle(wl, q, k)
     _compare(wl, q, k, v, gpu, orc)
+
+
+@pytest.mark.parametrize("scale", [0.06, 0.15])
+def test_caller_softmax_scale(scale):
+    """A softmax scale in the problem (instead of 1/sqrt(d)) reaches every
+    stage: block scores, last-block masses and the attention."""
+    U = _gpu()
+    wl = LLAMA.replace(seq_len=2600, num_q_heads=8, num_kv_heads=2, num_proxy_groups=2)
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl, softmax_scale=scale)
+    gpu = U.run_path(prob, q, k, v, wl.gamma, wl.min_budget_tokens)
+    orc = _oracle(wl, q, k, scale=scale)
+    _compare(wl, q, k, v, gpu, orc, scale=scale)
 
 
 def test_min_budget_and_full_budget():
