@@ -479,17 +479,16 @@ def test_whole_step_replays_from_a_hip_graph():
             assert torch.equal(getattr(bufs, n), ref[n]), f"replay {rep}: {n} differs"
 
 
-def test_256k_layer_sampled_rows():
-    """One layer of the 256K stack (layer 0) in the benchmark's launch
-    configuration: pooled heads bit-exact, every head's last-block mass and
-    budget, and the proxy scores, lists and attention of seeded sampled query
-    rows (always including the last row) and their block rows."""
+def _sampled_rows_check(wl, nsample: int):
+    """The whole path at full size, in the benchmark's launch configuration:
+    pooled heads bit-exact, every head's last-block mass and budget, and the
+    proxy scores, lists and attention of seeded sampled query rows (always
+    including the last row) and their block rows."""
     U = _gpu()
-    wl = WORKLOADS["llama3_8b_n262144"]
     q, k, v = U.inputs(wl)
     prob = U.problem_of(wl)
     rng = np.random.default_rng(12345)
-    rows = np.unique(np.concatenate([rng.integers(0, wl.seq_len, 32), [wl.seq_len - 1]]))
+    rows = np.unique(np.concatenate([rng.integers(0, wl.seq_len, nsample), [wl.seq_len - 1]]))
     brows = np.unique(rows // wl.block_size)
     gpu = U.run_path(prob, q, k, v, wl.gamma)
     sc = O.default_scale(wl.head_dim)
@@ -518,6 +517,20 @@ def test_256k_layer_sampled_rows():
     print(f"\n[{wl.name}] |dlogA|={dla:.2e} |dmass|/rows={dm:.2e} max|dO|={rep.max_abs:.2e} "
           f"mean|dO|={rep.mean_abs:.2e} |dlse|={dl:.2e} ambiguous heads={len(rep.ambiguous_heads)} "
           f"rows={rep.ambiguous_rows} of {rep.rows_checked}", flush=True)
+
+
+def test_256k_layer_sampled_rows():
+    """One layer of the 256K stack (layer 0), 32 sampled query rows."""
+    _sampled_rows_check(WORKLOADS["llama3_8b_n262144"], 32)
+
+
+def test_maximum_size_sampled_rows():
+    """The largest problem the library accepts: 8192 blocks of 128 tokens
+    (N = 1,048,576), with 4 query heads on one KV head and d = 64 to keep
+    the oracle's share small; 16 sampled query rows."""
+    wl = LLAMA.replace(seq_len=8192 * 128, num_q_heads=4, num_kv_heads=1, head_dim=64,
+                       num_proxy_groups=1, name="llama_shaped_n1048576_h4")
+    _sampled_rows_check(wl, 16)
 
 
 @pytest.mark.parametrize("name,rows_per_head", [("llama3_8b_n32768", 256),
