@@ -181,6 +181,33 @@ def test_caller_softmax_scale(scale):
     _compare(wl, q, k, v, gpu, orc, scale=scale)
 
 
+def test_all_zero_queries_give_exact_ties_to_lower_blocks():
+    """Q = 0: every proxy score is 0, so within a block row every causal key
+    block pools to the same value (the largest probability of a block's
+    rows is 1/(t'+1) of its first row, whichever key block).  The scores must
+    tie exactly, and every list must then be the lowest block indices
+    [0, 1, ..., K-1] (ties go to the lower index); attention as the oracle."""
+    U = _gpu()
+    wl = LLAMA.replace(seq_len=2048 + 40, num_q_heads=8, num_kv_heads=2, num_proxy_groups=2)
+    _, k, v = U.inputs(wl)
+    q = np.zeros((wl.seq_len, wl.num_q_heads, wl.head_dim), np.float32)
+    prob = U.problem_of(wl)
+    gpu = U.run_path(prob, q, k, v, wl.gamma)
+    la = gpu["logA"]
+    mq = la.shape[1]
+    for m in range(mq):
+        row = la[:, m, :m + 1]
+        assert np.all(row == row[:, :1]), f"block row {m}: scores do not tie exactly"
+        assert np.all(np.isneginf(la[:, m, m + 1:]))
+    for i in range(wl.num_q_heads):
+        for m in range(mq):
+            c = int(gpu["block_count"][i, m])
+            assert c == min(int(gpu["counts"][i]), m + 1)
+            assert np.array_equal(gpu["block_index"][i, m, :c], np.arange(c)), (i, m)
+    orc = _oracle(wl, q, k)
+    _compare(wl, q, k, v, gpu, orc)
+
+
 def test_min_budget_and_full_budget():
     U = _gpu()
     wl = LLAMA.replace(seq_len=4096, min_budget_tokens=2048)
