@@ -208,6 +208,19 @@ def test_all_zero_queries_give_exact_ties_to_lower_blocks():
     _compare(wl, q, k, v, gpu, orc)
 
 
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 17, 127, 128, 129, 255])
+def test_tiny_sequences(n):
+    """N below the stride (one strided token), below, at and just above one
+    block, and a ragged second block: the whole path against the oracle."""
+    U = _gpu()
+    wl = LLAMA.replace(seq_len=n, num_q_heads=8, num_kv_heads=2, num_proxy_groups=2)
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    gpu = U.run_path(prob, q, k, v, wl.gamma)
+    orc = _oracle(wl, q, k)
+    _compare(wl, q, k, v, gpu, orc)
+
+
 def test_min_budget_and_full_budget():
     U = _gpu()
     wl = LLAMA.replace(seq_len=4096, min_budget_tokens=2048)
