@@ -120,7 +120,6 @@ template <> __device__ __forceinline__ bf16 from_f32_rne<bf16>(float x) { return
 // 2^x on the hardware transcendental unit (v_exp_f32, ~1 ulp; no denormal
 // range fix-up, which the softmax does not need).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
 // Exchanges between the two wave halves without LDS: v_permlane32_swap of x
 // with itself gives, in every lane l, r[0] = x[l % 32] and r[1] = x[l % 32 + 32].
@@ -157,8 +156,6 @@ __device__ __forceinline__ uint32_t float_order_key(float f) {
     uint32_t u = __float_as_uint(f);
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
-
-__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // Index of the lower-triangular pair (m, n), n <= m.
 __device__ __forceinline__ int64_t tri_index(int m, int n) {
