@@ -52,6 +52,9 @@ def parse():
                                          "head_similarity_128k", "seq_len_llama"],
                     default=None,
                     help="print one JSON line per point of a workload sweep instead")
+    ap.add_argument("--work-orders", action="store_true",
+                    help="time the sparse attention call of --workload under each work-item "
+                         "order (one JSON line per order) instead")
     ap.add_argument("--stack", type=int, default=None, metavar="LAYERS",
                     help="time a stack of LAYERS layers of --workload (layer l drawn with seed l; "
                          "one JSON line per layer, then the totals)")
@@ -706,6 +709,65 @@ def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
         print(json.dumps(line), flush=True)
 
 
+# (PROXYATTN_ATTN_ORDER, PROXYATTN_ATTN_CHUNK_ROWS) points of --work-orders:
+# 0 = longest rows first, heads fastest; 1 = chunks of R rows x all heads;
+# 2 = chunks of R rows x the query heads of one KV head, KV head by KV head.
+WORK_ORDERS = [(0, 1), (1, 2), (1, 8), (2, 1), (2, 4), (2, 16), (2, 64)]
+
+
+def run_work_orders(wl, reps: int):
+    """Time the block-sparse call on one set of lists under each work-item
+    order of the library (its PROXYATTN_ATTN_ORDER / PROXYATTN_ATTN_CHUNK_ROWS
+    settings), one JSON line per order.  Launch sequence, which a rocprofv3
+    --pmc run of this mode sees in the same order: per order one untimed call,
+    then `reps` timed calls."""
+    import torch
+    from paper_2509_24745_amd import proxyattn as pa
+    from paper_2509_24745_amd.synth import generate
+
+    prob = pa.Problem(seq_len=wl.seq_len, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                      head_dim=wl.head_dim, block_size=wl.block_size,
+                      num_proxy_groups=wl.num_proxy_groups, stride=wl.stride, dtype=wl.dtype)
+    host = generate(wl)
+    q, k, v = (torch.from_numpy(host[x]).to(prob.torch_dtype).cuda() for x in ("q", "k", "v"))
+    del host
+    bufs = pa.Buffers(prob)
+    st = torch.cuda.current_stream()
+    pa.proxyattn_estimate(prob, q, k, bufs.logscore, bufs.mass, bufs.workspace, st)
+    pa.proxyattn_select_budget(prob, bufs.logscore, bufs.mass, wl.gamma, wl.min_budget_tokens,
+                               bufs.head_count, bufs.block_count, bufs.block_index, st)
+    torch.cuda.synchronize()
+    blocks = int(bufs.block_count.sum().item())
+    saved = {x: os.environ.get(x) for x in ("PROXYATTN_ATTN_ORDER", "PROXYATTN_ATTN_CHUNK_ROWS")}
+    try:
+        for order, rows in WORK_ORDERS:
+            os.environ["PROXYATTN_ATTN_ORDER"] = str(order)
+            os.environ["PROXYATTN_ATTN_CHUNK_ROWS"] = str(rows)
+            call = lambda: pa.proxyattn_block_sparse_prefill(
+                prob, q, k, v, bufs.block_count, bufs.block_index, bufs.out, None,
+                bufs.workspace, st)
+            call()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(reps):
+                call()
+            e1.record(st)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            print(json.dumps({"workload": wl.name, "attn_order": order, "chunk_rows": rows,
+                              "attn_ms": round(ms, 3), "reps": reps, "computed_blocks": blocks,
+                              "attn_tflops": round(4.0 * wl.block_size ** 2 * wl.head_dim *
+                                                   blocks / (ms * 1e-3) / 1e12, 1)}),
+                  flush=True)
+    finally:
+        for x, val in saved.items():
+            if val is None:
+                os.environ.pop(x, None)
+            else:
+                os.environ[x] = val
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -733,6 +795,9 @@ def main():
         return
     if args.sweep:
         run_sweep(args.sweep, args.steps, args.warmup, args.dense_steps)
+        return
+    if args.work_orders:
+        run_work_orders(WORKLOADS[args.workload], max(1, args.steps))
         return
 
     wl = WORKLOADS[args.workload]
