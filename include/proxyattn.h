@@ -38,6 +38,15 @@
  *  - Results are bitwise deterministic (no floating-point atomics).
  *  - N == 0 is a valid empty problem: nothing is enqueued.
  *  - Inputs must be finite; non-finite inputs give unspecified outputs.
+ *  - Two environment variables tune the order in which the attention kernel
+ *    takes its work items; results are bitwise the same under every setting.
+ *    PROXYATTN_ATTN_ORDER: 0 (longest block rows first, heads fastest),
+ *    1 (chunks of R block rows x all heads) or 2 (chunks of R block rows x
+ *    the query heads of one KV head, KV head by KV head).
+ *    PROXYATTN_ATTN_CHUNK_ROWS: R, an integer in [1, 8192].
+ *    Unset or empty selects the default, chosen by problem size.  Any other
+ *    value makes every call that takes a problem descriptor fail with
+ *    PROXYATTN_E_INVALID.
  */
 #ifndef PROXYATTN_H
 #define PROXYATTN_H
@@ -68,7 +77,7 @@ extern "C" {
  * 16-byte aligned.
  *
  * Supported: d in {64, 128}; b in {64, 128}; s in {1, 2, 4} with b/s >= 16;
- * Hq % Hkv == 0; Hq % G == 0; Nk <= 8192.  bf16 problems compute products on
+ * Hq <= 4096; Hq % Hkv == 0; Hq % G == 0; Nk <= 8192.  bf16 problems compute products on
  * bf16 MFMA with fp32 accumulation; fp32 problems on fp32 MFMA.
  */
 typedef struct proxyattn_problem {

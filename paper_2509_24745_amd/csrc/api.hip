@@ -3,6 +3,8 @@
 // arguments before enqueuing anything, never allocates and never
 // synchronises.
 #include <algorithm>
+#include <errno.h>
+#include <limits.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -33,9 +35,16 @@ static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Integer value of environment variable `name`: `dflt` when it is unset or
+// empty, INT_MIN when it is not a whole decimal integer in int range.
 static int env_int(const char* name, int dflt) {
     const char* v = getenv(name);
-    return (v && *v) ? atoi(v) : dflt;
+    if (!v || !*v) return dflt;
+    errno = 0;
+    char* end = nullptr;
+    const long x = strtol(v, &end, 10);
+    if (errno || end == v || *end || x < INT_MIN + 1 || x > INT_MAX) return INT_MIN;
+    return (int)x;
 }
 
 // Validates the descriptor and resolves it into a Shape.
@@ -49,6 +58,10 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
         return fail(PROXYATTN_E_INVALID, "head and group counts must be positive");
     if (p->head_dim <= 0 || p->block_size <= 0 || p->stride <= 0)
         return fail(PROXYATTN_E_INVALID, "head_dim, block_size and stride must be positive");
+    // grid y/z dimensions carry head and group counts, and the attention
+    // kernel's item numbers (about Hq * (Nk + 8R)) must fit an int
+    if (p->num_q_heads > 4096)
+        return fail(PROXYATTN_E_UNSUPPORTED, "num_q_heads %d > 4096", p->num_q_heads);
     if (p->num_q_heads % p->num_kv_heads)
         return fail(PROXYATTN_E_UNSUPPORTED, "num_q_heads %% num_kv_heads != 0");
     if (p->num_q_heads % p->num_proxy_groups)
@@ -125,6 +138,11 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
         const bool big = kvb_bytes > kMallBytes;
         s.attn_order = env_int("PROXYATTN_ATTN_ORDER", big ? 2 : 1);
         s.attn_chunk_rows = env_int("PROXYATTN_ATTN_CHUNK_ROWS", big ? 4 : 2);
+        // the item arithmetic multiplies R by head counts in int
+        if (s.attn_order < 0 || s.attn_order > 2)
+            return fail(PROXYATTN_E_INVALID, "PROXYATTN_ATTN_ORDER must be 0, 1 or 2");
+        if (s.attn_chunk_rows < 1 || s.attn_chunk_rows > 8192)
+            return fail(PROXYATTN_E_INVALID, "PROXYATTN_ATTN_CHUNK_ROWS must be an integer in [1, 8192]");
     }
     const int64_t strides[6] = {s.q_tok, s.q_head, s.kv_tok, s.kv_head, s.o_tok, s.o_head};
     for (int j = 0; j < 6; ++j) {

@@ -77,6 +77,8 @@ def test_version_and_error_strings():
     (dict(dtype="fp16"), pa.E_UNSUPPORTED),
     (dict(seq_len=8193 * 128), pa.E_UNSUPPORTED),   # more than 8192 blocks
     (dict(q_tok_stride=4100), pa.E_UNSUPPORTED),    # rows not 16-byte aligned
+    (dict(num_q_heads=4104, num_kv_heads=8, num_proxy_groups=8), pa.E_UNSUPPORTED),  # > 4096
+    (dict(num_q_heads=4096, num_kv_heads=8, num_proxy_groups=8), None),
 ])
 def test_problem_validation(kw, code):
     _lib()
@@ -87,6 +89,27 @@ def test_problem_validation(kw, code):
     with pytest.raises(pa.ProxyAttnError) as ei:
         pa.proxyattn_workspace_size(prob)
     assert ei.value.code == code
+
+
+@pytest.mark.parametrize("order,rows,ok", [
+    ("0", "1", True), ("1", "2", True), ("2", "8192", True), ("", "", True),
+    ("3", "4", False), ("-1", "4", False), ("2", "0", False), ("2", "-4", False),
+    ("2", "8193", False), ("2", "99999999999", False), ("2x", "4", False), ("2", "4.5", False),
+])
+def test_work_order_settings_are_validated(order, rows, ok, monkeypatch):
+    """The attention work-order knobs reach kernel index arithmetic: values
+    outside the documented ranges, or not integers, fail every call with
+    E_INVALID before anything is enqueued."""
+    _lib()
+    monkeypatch.setenv("PROXYATTN_ATTN_ORDER", order)
+    monkeypatch.setenv("PROXYATTN_ATTN_CHUNK_ROWS", rows)
+    if ok:
+        assert pa.proxyattn_workspace_size(_prob()) > 0
+        return
+    with pytest.raises(pa.ProxyAttnError) as ei:
+        pa.proxyattn_workspace_size(_prob())
+    assert ei.value.code == pa.E_INVALID
+    assert "PROXYATTN_ATTN_" in str(ei.value)
 
 
 def test_bad_struct_size_and_null_problem():
