@@ -28,8 +28,11 @@
  *  - Tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned.
  *    Problem descriptors and scalars are host values.
  *  - The library never allocates device memory and never synchronises.  Every
- *    call validates all of its arguments first; a call that returns an error
- *    has enqueued nothing.  A call that returns PROXYATTN_OK has enqueued its
+ *    call validates all of its arguments first; a call that returns
+ *    PROXYATTN_E_INVALID, PROXYATTN_E_UNSUPPORTED or PROXYATTN_E_WORKSPACE has
+ *    enqueued nothing.  PROXYATTN_E_HIP means that one of the call's launches
+ *    failed; kernels the call launched before it stay enqueued, and the
+ *    outputs are then unspecified.  A call that returns PROXYATTN_OK has enqueued its
  *    kernels, in order, on `stream` (a hipStream_t; NULL = the default stream)
  *    and returns without waiting.  Faults inside kernels surface at the
  *    caller's next synchronisation.
