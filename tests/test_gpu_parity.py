@@ -573,19 +573,26 @@ def test_maximum_size_sampled_rows():
     _sampled_rows_check(wl, 16)
 
 
-@pytest.mark.parametrize("name,rows_per_head", [("llama3_8b_n32768", 256),
-                                                ("llama3_8b_n131072", 64)])
-def test_full_size_lists_and_sampled_attention(name, rows_per_head):
+@pytest.mark.parametrize("name,kw,rows_per_head", [
+    ("llama3_8b_n32768", {}, 256),
+    ("llama3_8b_n131072", {}, 64),
+    # heterogeneous heads (half near-dense, half local + sink), 7 proxy groups
+    # of 4 query heads that straddle the 4 KV heads of 7, and a 2048-token
+    # minimum budget
+    ("qwen25_7b_n65536", {"num_proxy_groups": 7, "min_budget_tokens": 2048}, 128),
+], ids=["llama_n32768", "llama_n131072", "qwen_n65536_g7_beta2048"])
+def test_full_size_lists_and_sampled_attention(name, kw, rows_per_head):
     """Full-size layers in the launch configuration the benchmark times: every
     score, budget and list checked; attention on sampled query rows (seeded,
     always including the last row)."""
     U = _gpu()
-    wl = WORKLOADS[name]
+    wl = WORKLOADS[name].replace(**kw) if kw else WORKLOADS[name]
+    print(f"\n[full size] {wl}", flush=True)
     q, k, v = U.inputs(wl)
     prob = U.problem_of(wl)
     rng = np.random.default_rng(12345)
     rows = np.unique(np.concatenate([rng.integers(0, wl.seq_len, rows_per_head),
                                      [wl.seq_len - 1]]))
-    gpu = U.run_path(prob, q, k, v, wl.gamma)
+    gpu = U.run_path(prob, q, k, v, wl.gamma, wl.min_budget_tokens)
     orc = _oracle(wl, q, k)
     _compare(wl, q, k, v, gpu, orc, attn_rows=rows)
