@@ -559,9 +559,13 @@ def _sampled_rows_check(wl, nsample: int):
           f"rows={rep.ambiguous_rows} of {rep.rows_checked}", flush=True)
 
 
-def test_256k_layer_sampled_rows():
-    """One layer of the 256K stack (layer 0), 32 sampled query rows."""
-    _sampled_rows_check(WORKLOADS["llama3_8b_n262144"], 32)
+@pytest.mark.parametrize("layer", [0, 31])
+def test_256k_layer_sampled_rows(layer):
+    """The first and the last layer of the 256K stack (layer l is drawn with
+    seed l), 32 sampled query rows each."""
+    wl = WORKLOADS["llama3_8b_n262144"].replace(seed=layer)
+    print(f"\n[256K layer {layer}]", flush=True)
+    _sampled_rows_check(wl, 32)
 
 
 def test_maximum_size_sampled_rows():
