@@ -204,6 +204,25 @@ int proxyattn_block_sparse_prefill(const proxyattn_problem* p, const void* q, co
                                    const int32_t* block_index, void* out, float* lse,
                                    void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Checks caller-made lists against what proxyattn_block_sparse_prefill
+ * accepts: the lists of Eq. 3 (Sec. 3.2) select distinct causal key blocks
+ * n <= m of query block m.  For every head i and block row m writes
+ * status[i][m] (device [Hq][Mq] int32, out): 0 when
+ * 1 <= block_count[i][m] <= m+1 and the first block_count[i][m] entries of
+ * block_index[i][m] are distinct and lie in 0..m; otherwise the OR of
+ *   PROXYATTN_LIST_BAD_COUNT  count outside [1, m+1];
+ *   PROXYATTN_LIST_BAD_INDEX  an entry outside [0, m];
+ *   PROXYATTN_LIST_DUPLICATE  a block listed twice,
+ * where the entries examined are the first min(max(count, 0), Nk).  Reads
+ * nothing beyond those entries; deterministic; no workspace.
+ */
+#define PROXYATTN_LIST_BAD_COUNT 1
+#define PROXYATTN_LIST_BAD_INDEX 2
+#define PROXYATTN_LIST_DUPLICATE 4
+int proxyattn_check_lists(const proxyattn_problem* p, const int32_t* block_count,
+                          const int32_t* block_index, int32_t* status, void* stream);
+
 /* Dense causal attention with the same kernels (every block n <= m). */
 int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const void* k,
                             const void* v, void* out, float* lse, void* workspace,

@@ -313,6 +313,20 @@ int proxyattn_select_topk(const proxyattn_problem* p, const float* block_logscor
     return PROXYATTN_OK;
 }
 
+int proxyattn_check_lists(const proxyattn_problem* p, const int32_t* block_count,
+                          const int32_t* block_index, int32_t* status, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(block_count, "block_count"));
+    PA_TRY(check_ptr(block_index, "block_index"));
+    PA_TRY(check_ptr(status, "status"));
+    PA_LAUNCH(launch_check_lists(sh, block_count, block_index, status, (hipStream_t)stream),
+              "check_lists");
+    return PROXYATTN_OK;
+}
+
 static int prefill_common(const proxyattn_problem* p, const void* q, const void* k,
                           const void* v, const int32_t* block_count, const int32_t* block_index,
                           void* out, float* lse, void* workspace, size_t workspace_bytes,

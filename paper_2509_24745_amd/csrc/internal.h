@@ -90,6 +90,8 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
                          int row_ratio, int* block_count, int* block_index, hipStream_t st);
+hipError_t launch_check_lists(const Shape& sh, const int* block_count, const int* block_index,
+                              int* status, hipStream_t st);
 // launch_kv_block also resets the attention work queues; launch_attention
 // must follow it on the same stream.
 hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,

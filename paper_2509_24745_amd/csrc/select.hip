@@ -14,8 +14,10 @@
 //   i.e. the same fraction of every row's causal blocks).
 //   Rank order makes the lists of a group's heads prefixes of one another,
 //   so the attention workgroups of those heads, which run side by side on
-//   one XCD, fetch the same K/V blocks in the same order and share them
-//   through the L2.
+//   one XCD, fetch the same K/V blocks in the same order; blocks read close
+//   together in time are shared through the L2.
+// check_lists: one workgroup per (block row m, head i); validates a
+//   caller-made list against what the attention step accepts.
 #include "common.h"
 #include "internal.h"
 
@@ -156,6 +158,48 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
             out[p] = p < kk ? (int)(key[p] & 0xffffffffu) : -1;
         if (tid == 0) block_count[(int64_t)i * sh.mq + m] = kk;
     }
+}
+
+// Status of list (i, m): bit 0 = count outside [1, m+1]; bit 1 = one of the
+// first min(max(count, 0), Nk) entries outside [0, m]; bit 2 = a block listed
+// twice among them.  A bitmap of the row's m+1 causal blocks in LDS finds
+// the duplicates (integer LDS atomics: the result does not depend on which
+// thread sees the second copy).
+constexpr int kCheckThreads = 256;
+
+__global__ __launch_bounds__(kCheckThreads) void check_lists_kernel(
+    Shape sh, const int* __restrict__ block_count, const int* __restrict__ block_index,
+    int* __restrict__ status) {
+    __shared__ unsigned seen[8192 / 32];
+    __shared__ int flags;
+    const int m = blockIdx.x, i = blockIdx.y, tid = threadIdx.x, nk = sh.mq;
+    for (int wd = tid; wd < (m + 32) / 32; wd += kCheckThreads) seen[wd] = 0u;
+    if (tid == 0) flags = 0;
+    __syncthreads();
+    const int64_t row = (int64_t)i * sh.mq + m;
+    const int cnt = block_count[row];
+    const int n = min(max(cnt, 0), nk);
+    const int* list = block_index + row * nk;
+    int f = (cnt < 1 || cnt > m + 1) ? 1 : 0;
+    for (int p = tid; p < n; p += kCheckThreads) {
+        const int v = list[p];
+        if (v < 0 || v > m) {
+            f |= 2;
+        } else {
+            const unsigned bit = 1u << (v & 31);
+            if (atomicOr(&seen[v >> 5], bit) & bit) f |= 4;
+        }
+    }
+    if (f) atomicOr(&flags, f);
+    __syncthreads();
+    if (tid == 0) status[row] = flags;
+}
+
+hipError_t launch_check_lists(const Shape& sh, const int* block_count, const int* block_index,
+                              int* status, hipStream_t st) {
+    hipLaunchKernelGGL(check_lists_kernel, dim3(sh.mq, sh.hq), dim3(kCheckThreads), 0, st, sh,
+                       block_count, block_index, status);
+    return hipGetLastError();
 }
 
 hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,

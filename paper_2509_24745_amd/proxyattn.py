@@ -23,6 +23,7 @@ F32 = 1
 
 E_OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, 1, 2, 3, 4
 TOPK_CONSTANT, TOPK_ROW_RATIO = 0, 1
+LIST_BAD_COUNT, LIST_BAD_INDEX, LIST_DUPLICATE = 1, 2, 4
 
 
 class proxyattn_problem(ctypes.Structure):
@@ -61,6 +62,7 @@ _SIGS = {
     "proxyattn_head_overlap": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p],
+    "proxyattn_check_lists": [ctypes.c_void_p] * 5,
     "proxyattn_block_sparse_prefill": [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_dense_prefill": [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_error_string": [ctypes.c_int],
@@ -292,6 +294,14 @@ def proxyattn_head_overlap(prob: Problem, q, k, query_token: int, topk: int, sin
                                         _ptr(scores), _ptr(workspace),
                                         _nbytes(workspace) if workspace is not None else 0,
                                         _stream(stream)))
+
+
+def proxyattn_check_lists(prob: Problem, block_count, block_index, status, stream=None):
+    _need_lists(prob, block_count, block_index)
+    _need(status, prob.num_q_heads * prob.num_blocks, "status", torch.int32)
+    p = prob.c_struct()
+    _check(lib().proxyattn_check_lists(ctypes.byref(p), _ptr(block_count), _ptr(block_index),
+                                       _ptr(status), _stream(stream)))
 
 
 def proxyattn_block_sparse_prefill(prob: Problem, q, k, v, block_count, block_index, out, lse,

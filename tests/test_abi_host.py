@@ -199,6 +199,10 @@ def test_calls_reject_bad_arguments_before_launch():
     for gamma, beta in ((0.0, 0), (1.5, 0), (float("nan"), 0), (0.9, -1)):
         assert lib.proxyattn_budget(ctypes.byref(p), fake, gamma, beta, fake, None) == pa.E_INVALID
     assert lib.proxyattn_budget(ctypes.byref(p), fake, 0.9, 0, None, None) == pa.E_INVALID
+    # list check: null or misaligned pointers
+    assert lib.proxyattn_check_lists(ctypes.byref(p), fake, fake, None, None) == pa.E_INVALID
+    assert lib.proxyattn_check_lists(ctypes.byref(p), None, fake, fake, None) == pa.E_INVALID
+    assert lib.proxyattn_check_lists(ctypes.byref(p), fake, fake + 4, fake, None) == pa.E_INVALID
     # unknown top-k mode, missing counts
     for mode in (-1, 2, 7):
         assert lib.proxyattn_select_topk(ctypes.byref(p), fake, fake, mode, fake, fake, None) \

@@ -385,6 +385,93 @@ def test_work_orders_give_identical_output(wl, monkeypatch):
             assert torch.equal(lse, ref[dense][1]), (order, rows, dense)
 
 
+def _list_status(bc, bi):
+    """What proxyattn_check_lists reports, row by row in NumPy."""
+    hq, mq = bc.shape
+    st = np.zeros((hq, mq), np.int32)
+    for i in range(hq):
+        for m in range(mq):
+            c = int(bc[i, m])
+            f = 0 if 1 <= c <= m + 1 else 1
+            ent = bi[i, m, :min(max(c, 0), mq)]
+            inside = ent[(ent >= 0) & (ent <= m)]
+            if inside.size != ent.size:
+                f |= 2
+            if np.unique(inside).size != inside.size:
+                f |= 4
+            st[i, m] = f
+    return st
+
+
+def test_check_lists_flags_every_malformed_row():
+    """Selected lists are clean; caller lists with planted faults (counts out
+    of range, entries out of the causal range, repeated blocks, padding
+    beyond the count that must not be read) are flagged exactly."""
+    U = _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    wl = LLAMA.replace(seq_len=40 * 64 + 17, block_size=64, num_q_heads=8, num_kv_heads=2,
+                       num_proxy_groups=2)
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    gpu = U.run_path(prob, q, k, v, wl.gamma)
+    hq, mq = gpu["block_count"].shape
+
+    def run(bc, bi):
+        st = torch.full((hq, mq), -7, dtype=torch.int32, device="cuda")
+        pa.proxyattn_check_lists(prob, torch.from_numpy(bc).cuda(), torch.from_numpy(bi).cuda(),
+                                 st)
+        torch.cuda.synchronize()
+        return st.cpu().numpy()
+
+    bc, bi = gpu["block_count"].copy(), gpu["block_index"].copy()
+    assert not run(bc, bi).any(), "selected lists flagged"
+    rng = np.random.default_rng(7)
+    bc2, bi2 = bc.copy(), bi.copy()
+    for _ in range(60):
+        i, m = int(rng.integers(hq)), int(rng.integers(mq))
+        kind = int(rng.integers(5))
+        c = min(max(int(bc2[i, m]), 0), mq)   # entries the check examines
+        if kind == 0:
+            bc2[i, m] = int(rng.choice([0, -3, m + 2, mq + 5]))
+        elif kind == 1 and c >= 1:
+            bi2[i, m, int(rng.integers(c))] = int(rng.choice([-1, m + 1, mq + 9]))
+        elif kind == 2 and c >= 2:
+            a, b = rng.choice(c, 2, replace=False)
+            bi2[i, m, b] = bi2[i, m, a]
+        elif kind == 3:
+            bi2[i, m, c:] = 0          # junk past the count: not read
+        elif kind == 4 and 1 <= c <= m:
+            bc2[i, m] = c + 1          # one more entry: the -1 padding
+    want = _list_status(bc2, bi2)
+    got = run(bc2, bi2)
+    assert want.any()
+    assert np.array_equal(got, want), np.argwhere(got != want)[:5]
+
+
+def test_check_lists_at_the_largest_size():
+    """8192 blocks (the LDS bitmap's full width): full causal lists are clean;
+    planted faults in the last rows are flagged."""
+    _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    mq, b = 8192, 64
+    prob = pa.Problem(seq_len=mq * b, num_q_heads=1, num_kv_heads=1, head_dim=64, block_size=b,
+                      num_proxy_groups=1, stride=4, dtype="bf16")
+    bc = np.arange(1, mq + 1, dtype=np.int32)[None, :]
+    bi = np.full((1, mq, mq), -1, dtype=np.int32)
+    tri = np.tril_indices(mq)
+    bi[0][tri] = tri[1]
+    bi[0, mq - 1, mq - 1] = mq - 2      # duplicate in the last row
+    bi[0, 5000, 17] = 5001               # beyond the causal range
+    bc[0, 6000] = 0                      # empty list
+    st = torch.full((1, mq), -7, dtype=torch.int32, device="cuda")
+    pa.proxyattn_check_lists(prob, torch.from_numpy(bc).cuda(), torch.from_numpy(bi).cuda(), st)
+    torch.cuda.synchronize()
+    got = st.cpu().numpy()[0]
+    want = np.zeros(mq, np.int32)
+    want[mq - 1], want[5000], want[6000] = 4, 2, 1
+    assert np.array_equal(got, want), np.argwhere(got != want)[:5]
+
+
 def test_empty_problem_is_a_noop():
     _gpu()
     from paper_2509_24745_amd import proxyattn as pa
