@@ -29,8 +29,12 @@
 //   - the scores of step j+1 (MFMA) are interleaved instruction by
 //     instruction with the softmax of step j (VALU), then PV of step j runs,
 //     as one explicit software pipeline in which every LDS fragment read is
-//     issued two MFMAs ahead of its use; the row max of step j+1 closes the
-//     step, so the rare rescale branch stays out of that block.
+//     issued two MFMAs ahead of its use;
+//   - the probability sum of step j and the row maxima of step j+1 are
+//     computed inside the PV segments (held there by empty asm operands, so
+//     that the optimizer cannot sink them past the masking branch); a masked
+//     sub-tile (the diagonal block or a ragged end) takes its maxima again
+//     after masking, and the rare rescale branch stays outside the block.
 #include <algorithm>
 #include <mutex>
 #include <vector>
