@@ -352,6 +352,7 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
     t_est = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     t_sel = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    per_step = [e[0].elapsed_time(e[3]) for e in evs]   # estimate start to attention end
     print(f"[bench] {wl.name}: {ms_total:.3f} ms/step (est {t_est:.3f}, sel {t_sel:.3f}, "
           f"attn {t_attn:.3f})", file=sys.stderr, flush=True)
 
@@ -415,6 +416,8 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
                   "p01_row": float(torch.quantile(rec.flatten()[::97].float(), 0.01))}
     res = {
         "ms_total": ms_total, "t_est": t_est, "t_sel": t_sel, "t_attn": t_attn, "t_dense": t_dense,
+        "step_median": float(np.median(per_step)) if per_step else None,
+        "step_min": float(np.min(per_step)) if per_step else None,
         "sparsity": 1.0 - total_blocks / causal_blocks, "total_blocks": total_blocks,
         "f_dense": f_dense, "f_attn": f_attn, "achieved": achieved, "peak": peak,
         "head_count_min": int(counts.min()), "head_count_median": float(np.median(counts)),
@@ -859,6 +862,8 @@ def main():
         "t_estimate_ms": round(t_est, 4),
         "t_select_ms": round(t_sel, 4),
         "t_attention_ms": round(t_attn, 4),
+        "step_ms_median": round(r["step_median"], 4) if r["step_median"] is not None else None,
+        "step_ms_min": round(r["step_min"], 4) if r["step_min"] is not None else None,
         "graph_replay_ms_per_step": round(r["t_graph"], 4) if r["t_graph"] else None,
         "torch_sdpa_flash_ms": round(t_vendor, 3) if t_vendor else None,
         "speedup_vs_torch_sdpa_flash": round(t_vendor / ms_total, 3) if t_vendor else None,
