@@ -62,6 +62,9 @@ CASES = {
     "llama_g32_n2048": LLAMA.replace(seq_len=2048, num_proxy_groups=32),
     "qwen_g7_n8192": QWEN.replace(seq_len=8192, num_proxy_groups=7),
     "llama_n100_single_partial_block": LLAMA.replace(seq_len=100),
+    # the first block of every sorted mass already exceeds gamma: one block
+    # per head, so every row keeps only its top-ranked block
+    "llama_gamma_tiny_n2048": LLAMA.replace(seq_len=2048, gamma=1e-6),
     "fp32_d128_b128_n1000": LLAMA.replace(seq_len=1000, dtype="fp32", num_q_heads=8,
                                           num_kv_heads=2, num_proxy_groups=2),
     # the remaining compiled (dtype, d, b) instantiations; b = 64 with d = 128
