@@ -463,3 +463,81 @@ def test_shared_ranking_curves_reduce_to_own_ranking_for_identical_heads():
     q2 = rng.standard_normal((n, 3, 8)).astype(np.float32)
     shared, own = O.shared_ranking_curves(q2, k, t, 0.4, [1, 8, 64, 128])
     assert np.all(shared <= own + 1e-12)                  # the own ranking is optimal
+
+
+# ------------------------------------------------------ GQA head mapping and softmax scale
+# References below come from torch's scaled_dot_product_attention in float64
+# with enable_gqa=True: the library repeats each KV head over its
+# Hq/Hkv consecutive query heads itself, and takes the scale as an argument.
+# Every case has Hq/Hkv = 2 or 3 with distinct KV heads, nonzero queries and
+# a scale other than 1/sqrt(d), so reading KV head i % Hkv instead of
+# i // (Hq/Hkv), or dropping the scale, fails each of them (both mutations
+# were applied to a copy of the oracle and made every one of these fail).
+def _sdpa_f64(q, k, v, scale, causal):
+    """q [Hq, Tq, d], k [Hkv, Tk, d], v [Hkv, Tk, e] -> [Hq, Tq, e], float64."""
+    import torch
+    import torch.nn.functional as F
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))[None]
+    o = F.scaled_dot_product_attention(t(q), t(k), t(v), is_causal=causal, scale=float(scale),
+                                       enable_gqa=True)
+    return o[0].numpy()
+
+
+def _sdpa_token_probs(q, k, t, scale):
+    """Probabilities of query token t over keys 0..t for every head: SDPA
+    with V = the identity, so the output rows are the softmax rows."""
+    hkv = k.shape[1]
+    eye = np.broadcast_to(np.eye(t + 1), (hkv, t + 1, t + 1))
+    return _sdpa_f64(q[t:t + 1].transpose(1, 0, 2), k[:t + 1].transpose(1, 0, 2), eye, scale,
+                     causal=False)[:, 0, :]
+
+
+@pytest.mark.parametrize("hq,hkv,t", [(6, 2, 37), (4, 2, 1), (6, 3, 59)])
+def test_token_attention_gqa_and_scale_match_sdpa(hq, hkv, t):
+    q, k, _ = _qkv(60, hq, hkv, 16, scale=1.5, seed=21)
+    scale = 0.37                                      # 1/sqrt(16) = 0.25
+    got = O.token_attention(q, k, t, scale)
+    want = _sdpa_token_probs(q, k, t, scale)
+    assert got.shape == want.shape == (hq, t + 1)
+    assert np.allclose(got, want, rtol=2e-5, atol=1e-7)
+
+
+@pytest.mark.parametrize("sink,renorm", [(0, False), (3, False), (3, True)])
+def test_head_overlap_matches_brute_force_topk_sums_of_sdpa(sink, renorm):
+    """Eq. 4 by brute force on the float64 reference probabilities: for each
+    head i the k tokens with the largest probability, then every head's mass
+    on them (after the sink removal and renormalisation the call asks for)."""
+    hq, hkv, n, t, topk = 6, 2, 120, 97, 11
+    q, k, _ = _qkv(n, hq, hkv, 16, scale=1.5, seed=22)
+    scale = 0.31
+    a = _sdpa_token_probs(q, k, t, scale)
+    a[:, :sink] = 0.0
+    if renorm:
+        a = a / a.sum(axis=1, keepdims=True)
+    want = np.empty((hq, hq))
+    for i in range(hq):
+        order = sorted(range(t + 1), key=lambda u: (-a[i, u], u))
+        # the ranking is not decided by rounding: the k-th and (k+1)-th
+        # probabilities are far apart compared to fp32's error
+        assert a[i, order[topk - 1]] - a[i, order[topk]] > 1e-5
+        want[i] = a[:, order[:topk]].sum(axis=1)
+    got = O.head_overlap(q, k, t, topk, scale, sink_tokens=sink, renormalize=renorm)
+    assert np.allclose(got, want, rtol=1e-5, atol=1e-7)
+
+
+@pytest.mark.parametrize("n,b,hq,hkv", [(200, 32, 4, 2), (256, 64, 6, 2), (100, 64, 6, 3)])
+def test_lastblock_mass_gqa_and_scale_match_sdpa(n, b, hq, hkv):
+    """Alg. 1, first two steps: causal SDPA over the whole sequence with V =
+    the key-block indicator (V[u, n] = 1 when key u lies in block n) gives,
+    for every query row, its attention mass per key block; the mass is the
+    sum of those rows over the last min(b, N) query tokens."""
+    q, k, _ = _qkv(n, hq, hkv, 16, scale=1.5, seed=23)
+    scale = 0.41
+    nk = -(-n // b)
+    ind = np.zeros((n, nk))
+    ind[np.arange(n), np.arange(n) // b] = 1.0
+    per_row = _sdpa_f64(q.transpose(1, 0, 2), k.transpose(1, 0, 2),
+                        np.broadcast_to(ind, (hkv, n, nk)), scale, causal=True)
+    want = per_row[:, max(0, n - b):, :].sum(axis=1)
+    got = O.lastblock_mass(q, k, b, scale)
+    assert np.allclose(got, want, rtol=2e-5, atol=2e-6)
