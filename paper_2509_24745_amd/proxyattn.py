@@ -191,12 +191,15 @@ def proxyattn_workspace_layout(prob: Problem):
     return a.value, b.value
 
 
-# Size checks of torch arguments: the library receives raw pointers and
-# cannot see the allocations, so a tensor smaller than the problem would be
-# read or written out of bounds.  Each check needs the number of elements the
-# call touches from the tensor's data pointer (ints are raw pointers and are
-# passed through unchecked).
-def _need(x, n_elems: int, name: str, dtype=None):
+# Checks of torch arguments: the library receives raw pointers and cannot see
+# the allocations, so a tensor smaller than the problem would be read or
+# written out of bounds, and a host tensor's address would reach a kernel as
+# if it were device memory.  Each check needs the number of elements the call
+# touches from the tensor's data pointer (ints are raw pointers and are passed
+# through unchecked).  Q, K, V and O may be strided views (the problem carries
+# their strides); every other array is read as packed, so it must be
+# contiguous.
+def _need(x, n_elems: int, name: str, dtype=None, contiguous: bool = True):
     if x is None or isinstance(x, int) or n_elems <= 0:
         return
     if dtype is not None and x.dtype != dtype:
@@ -205,6 +208,25 @@ def _need(x, n_elems: int, name: str, dtype=None):
     if avail < n_elems:
         raise ProxyAttnError(E_INVALID, f"{name}: {avail} elements from its data pointer, the "
                                         f"problem touches {n_elems}")
+    if contiguous and not x.is_contiguous():
+        raise ProxyAttnError(E_INVALID, f"{name}: not contiguous (read as a packed array)")
+    if not x.is_cuda:
+        raise ProxyAttnError(E_INVALID, f"{name}: tensor on {x.device}, the library needs "
+                                        f"device memory of the current GPU")
+    if x.device.index != torch.cuda.current_device():
+        raise ProxyAttnError(E_INVALID, f"{name}: tensor on {x.device}, the current device is "
+                                        f"cuda:{torch.cuda.current_device()}")
+
+
+def _need_ws(workspace, n_bytes: int, name: str = "workspace"):
+    """A workspace of at least n_bytes on the current GPU (sizes are checked
+    again by the library against what the problem needs)."""
+    if workspace is None or isinstance(workspace, int):
+        return
+    _need(workspace, 1, name)
+    if workspace.numel() * workspace.element_size() < n_bytes:
+        raise ProxyAttnError(E_WORKSPACE, f"{name}: {workspace.numel() * workspace.element_size()}"
+                                          f" bytes, the problem needs {n_bytes}")
 
 
 def _span(n, heads, d, tok_stride, head_stride):
@@ -215,17 +237,17 @@ def _span(n, heads, d, tok_stride, head_stride):
 
 def _need_q(prob: Problem, q, name="q"):
     _need(q, _span(prob.seq_len, prob.num_q_heads, prob.head_dim, prob.q_tok_stride,
-                   prob.q_head_stride), name, prob.torch_dtype)
+                   prob.q_head_stride), name, prob.torch_dtype, contiguous=False)
 
 
 def _need_kv(prob: Problem, x, name):
     _need(x, _span(prob.seq_len, prob.num_kv_heads, prob.head_dim, prob.kv_tok_stride,
-                   prob.kv_head_stride), name, prob.torch_dtype)
+                   prob.kv_head_stride), name, prob.torch_dtype, contiguous=False)
 
 
 def _need_out(prob: Problem, out):
     _need(out, _span(prob.seq_len, prob.num_q_heads, prob.head_dim, prob.o_tok_stride,
-                     prob.o_head_stride), "out", prob.torch_dtype)
+                     prob.o_head_stride), "out", prob.torch_dtype, contiguous=False)
 
 
 def _need_scores(prob: Problem, block_logscore):
@@ -244,6 +266,7 @@ def proxyattn_estimate(prob: Problem, q, k, block_logscore, lastblk_mass, worksp
     _need_kv(prob, k, "k")
     _need_scores(prob, block_logscore)
     _need(lastblk_mass, prob.num_q_heads * prob.num_blocks, "lastblk_mass", torch.float32)
+    _need_ws(workspace, 0)
     p = prob.c_struct()
     _check(lib().proxyattn_estimate(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(block_logscore),
                                     _ptr(lastblk_mass), _ptr(workspace), _nbytes(workspace)
@@ -288,6 +311,7 @@ def proxyattn_head_overlap(prob: Problem, q, k, query_token: int, topk: int, sin
     _need_q(prob, q)
     _need_kv(prob, k, "k")
     _need(scores, prob.num_q_heads * prob.num_q_heads, "scores", torch.float32)
+    _need_ws(workspace, 0)
     p = prob.c_struct()
     _check(lib().proxyattn_head_overlap(ctypes.byref(p), _ptr(q), _ptr(k), int(query_token),
                                         int(topk), int(sink_tokens), int(bool(renormalize)),
@@ -312,6 +336,7 @@ def proxyattn_block_sparse_prefill(prob: Problem, q, k, v, block_count, block_in
     _need_lists(prob, block_count, block_index)
     _need_out(prob, out)
     _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
+    _need_ws(workspace, 0)
     p = prob.c_struct()
     _check(lib().proxyattn_block_sparse_prefill(
         ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(block_count), _ptr(block_index),
@@ -325,6 +350,7 @@ def proxyattn_dense_prefill(prob: Problem, q, k, v, out, lse, workspace, stream=
     _need_kv(prob, v, "v")
     _need_out(prob, out)
     _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
+    _need_ws(workspace, 0)
     p = prob.c_struct()
     _check(lib().proxyattn_dense_prefill(
         ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(workspace),

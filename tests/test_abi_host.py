@@ -235,28 +235,64 @@ def test_calls_reject_bad_arguments_before_launch():
 
 def test_binding_rejects_tensors_smaller_than_the_problem():
     """The library sees raw pointers only; the binding checks torch arguments
-    against the problem before any call (CPU tensors: nothing is launched)."""
+    against the problem before any call (CPU tensors: nothing is launched).
+    Arguments before the one under test are raw pointers (ints), which the
+    binding passes through unchecked."""
     import torch
     _lib()
     prob = _prob(seq_len=1000)
     n, hq, hkv, d = prob.seq_len, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
     mq = prob.num_blocks
     bf = torch.bfloat16
+    fake = 1 << 20
     q = torch.zeros(n, hq, d, dtype=bf)
-    k = torch.zeros(n, hkv, d, dtype=bf)
     small_k = torch.zeros(n // 2, hkv, d, dtype=bf)
     scores = torch.zeros(prob.num_proxy_groups, mq, mq)
     mass = torch.zeros(hq, mq)
     with pytest.raises(pa.ProxyAttnError, match="k: .* touches"):
-        pa.proxyattn_estimate(prob, q, small_k, scores, mass, None)
+        pa.proxyattn_estimate(prob, fake, small_k, scores, mass, None)
     with pytest.raises(pa.ProxyAttnError, match="dtype"):
-        pa.proxyattn_estimate(prob, q.float(), k, scores, mass, None)
-    bc = torch.zeros(hq, mq, dtype=torch.int32)
+        pa.proxyattn_estimate(prob, q.float(), fake, scores, mass, None)
     bi64 = torch.zeros(hq, mq, mq, dtype=torch.int64)
     with pytest.raises(pa.ProxyAttnError, match="block_index: dtype"):
-        pa.proxyattn_block_sparse_prefill(prob, q, k, k, bc, bi64, q, None, None)
+        pa.proxyattn_block_sparse_prefill(prob, fake, fake, fake, fake, bi64, fake, None, None)
     # a view offset into a larger buffer counts only what lies past its start
     big = torch.zeros(2 * n * hq * d, dtype=bf)
     tail_view = big[n * hq * d + 1:]
     with pytest.raises(pa.ProxyAttnError, match="out: .* touches"):
-        pa.proxyattn_dense_prefill(prob, q, k, k, tail_view, None, None)
+        pa.proxyattn_dense_prefill(prob, fake, fake, fake, tail_view, None, None)
+
+
+def test_binding_rejects_host_and_strided_tensors():
+    """A host tensor's address must never reach a kernel, and every array
+    other than Q, K, V and O is read as packed: full-size CPU tensors and
+    non-contiguous views are rejected before anything is launched."""
+    import torch
+    _lib()
+    prob = _prob(seq_len=1000)
+    n, hq, hkv, d = prob.seq_len, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    mq, g = prob.num_blocks, prob.num_proxy_groups
+    fake = 1 << 20
+    i32 = torch.int32
+    q = torch.zeros(n, hq, d, dtype=torch.bfloat16)
+    with pytest.raises(pa.ProxyAttnError, match="q: tensor on cpu"):
+        pa.proxyattn_estimate(prob, q, fake, fake, fake, fake)
+    with pytest.raises(pa.ProxyAttnError, match="head_count: tensor on cpu"):
+        pa.proxyattn_select_topk(prob, fake, torch.zeros(hq, dtype=i32), 0, fake, fake)
+    with pytest.raises(pa.ProxyAttnError, match="block_index: tensor on cpu"):
+        pa.proxyattn_block_sparse_prefill(prob, fake, fake, fake, fake,
+                                          torch.zeros(hq, mq, mq, dtype=i32), fake, None, fake)
+    with pytest.raises(pa.ProxyAttnError, match="workspace: tensor on cpu"):
+        pa.proxyattn_dense_prefill(prob, fake, fake, fake, fake, None,
+                                   torch.zeros(64, dtype=torch.uint8))
+    # strided views of packed arrays: a transposed score matrix, every other
+    # row of a list array, a column of a status matrix
+    scores_t = torch.zeros(g, mq, mq).transpose(1, 2)
+    with pytest.raises(pa.ProxyAttnError, match="block_logscore: not contiguous"):
+        pa.proxyattn_select_topk(prob, scores_t, fake, 0, fake, fake)
+    bc_every_other = torch.zeros(hq, 2 * mq, dtype=i32)[:, ::2]
+    with pytest.raises(pa.ProxyAttnError, match="block_count: not contiguous"):
+        pa.proxyattn_check_lists(prob, bc_every_other, fake, fake)
+    mass_t = torch.zeros(mq, hq).t()
+    with pytest.raises(pa.ProxyAttnError, match="lastblk_mass: not contiguous"):
+        pa.proxyattn_budget(prob, mass_t, 0.9, 0, fake)
