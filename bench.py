@@ -1,7 +1,10 @@
 """Benchmark of the ProxyAttn prefill hot path on one MI355X.
 
 One step = the whole path on one synthetic layer already resident in HBM:
-proxyattn_estimate -> proxyattn_select_budget -> proxyattn_block_sparse_prefill.
+proxyattn_estimate -> proxyattn_select_budget -> proxyattn_prepare_kv ->
+proxyattn_block_sparse_prefill_blocked.  The dense baseline runs the same
+attention kernel over every causal block on the step's K/V copy; its time
+includes one copy as well.
 Default workload: Llama-3-8B-shaped attention layer at 131072 tokens (32 query
 / 8 KV heads, d 128, block 128, 4 proxy groups, stride 4, gamma 0.95, head
 deviation 0.3), bf16.
@@ -326,6 +329,12 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         pa.proxyattn_select_topk(prob, bufs.logscore, bufs.head_count, mode, bufs.block_count,
                                  bufs.block_index, st)
 
+    # the K/V copy the attention kernels read: made once per step from the
+    # layer's K and V (proxyattn_prepare_kv), then read by the sparse call
+    # and, outside the step, by the dense baseline
+    kvb = torch.empty(pa.proxyattn_kv_blocked_size(prob), dtype=torch.uint8, device="cuda")
+    qws = torch.empty(pa.proxyattn_blocked_workspace_size(prob), dtype=torch.uint8, device="cuda")
+
     def step(ev=None, st=None):
         st = stream if st is None else st
         if ev: ev[0].record(st)
@@ -333,14 +342,16 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         if ev: ev[1].record(st)
         select(st)
         if ev: ev[2].record(st)
-        pa.proxyattn_block_sparse_prefill(prob, q, k, v, bufs.block_count, bufs.block_index,
-                                          bufs.out, bufs.lse, bufs.workspace, st)
+        pa.proxyattn_prepare_kv(prob, k, v, kvb, st)
         if ev: ev[3].record(st)
+        pa.proxyattn_block_sparse_prefill_blocked(prob, q, kvb, bufs.block_count,
+                                                  bufs.block_index, bufs.out, bufs.lse, qws, st)
+        if ev: ev[4].record(st)
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
@@ -351,10 +362,11 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
     ms_total = start.elapsed_time(stop) / steps
     t_est = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     t_sel = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    t_attn = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    per_step = [e[0].elapsed_time(e[3]) for e in evs]   # estimate start to attention end
+    t_prep = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    t_attn = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
+    per_step = [e[0].elapsed_time(e[4]) for e in evs]   # estimate start to attention end
     print(f"[bench] {wl.name}: {ms_total:.3f} ms/step (est {t_est:.3f}, sel {t_sel:.3f}, "
-          f"attn {t_attn:.3f})", file=sys.stderr, flush=True)
+          f"prep {t_prep:.3f}, attn {t_attn:.3f})", file=sys.stderr, flush=True)
 
     mq, hq, d, b, n = prob.num_blocks, prob.num_q_heads, prob.head_dim, prob.block_size, prob.seq_len
     total_blocks = int(bufs.block_count.sum().item())
@@ -390,21 +402,25 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         if not torch.equal(bufs.block_count, ref_count):
             raise RuntimeError("graph replay differs from the eager step")
         del graph
-    t_dense = None
+    t_dense = t_dense_attn = None
     if with_dense:
+        # the dense kernel on the K/V copy of the last step; its time adds the
+        # copy's, so that both sides include one proxyattn_prepare_kv
         de = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         dense_out = torch.empty_like(bufs.out)
-        pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
+        pa.proxyattn_dense_prefill_blocked(prob, q, kvb, dense_out, None, qws, stream)
         torch.cuda.synchronize()
         de[0].record(stream)
         for _ in range(dense_steps):
-            pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, None, bufs.workspace, stream)
+            pa.proxyattn_dense_prefill_blocked(prob, q, kvb, dense_out, None, qws, stream)
         de[1].record(stream)
         torch.cuda.synchronize()
-        t_dense = de[0].elapsed_time(de[1]) / dense_steps
-        print(f"[bench] dense {t_dense:.3f} ms", file=sys.stderr, flush=True)
+        t_dense_attn = de[0].elapsed_time(de[1]) / dense_steps
+        t_dense = t_prep + t_dense_attn
+        print(f"[bench] dense {t_dense_attn:.3f} ms (+ prep {t_prep:.3f})", file=sys.stderr,
+              flush=True)
         dense_lse = torch.empty_like(bufs.lse)
-        pa.proxyattn_dense_prefill(prob, q, k, v, dense_out, dense_lse, bufs.workspace, stream)
+        pa.proxyattn_dense_prefill_blocked(prob, q, kvb, dense_out, dense_lse, qws, stream)
         torch.cuda.synchronize()
         del dense_out
     recall = None
@@ -422,8 +438,9 @@ def measure(wl, steps: int, warmup: int, dense_steps: int, with_dense: bool = Tr
         "f_dense": f_dense, "f_attn": f_attn, "achieved": achieved, "peak": peak,
         "head_count_min": int(counts.min()), "head_count_median": float(np.median(counts)),
         "head_count_max": int(counts.max()),
-        "dense_mfma_frac": (4.0 * b * b * d * causal_blocks / (t_dense * 1e-3) / 1e12 / peak)
-        if t_dense else None,
+        "dense_mfma_frac": (4.0 * b * b * d * causal_blocks / (t_dense_attn * 1e-3) / 1e12 / peak)
+        if t_dense_attn else None,
+        "t_prep": t_prep, "t_dense_attn": t_dense_attn,
         "variant": variant, "static_k": static_k, "recall": recall, "t_graph": t_graph,
         "head_count_mean": float(counts.mean()), "dense_lse": dense_lse,
     }
@@ -436,7 +453,8 @@ def summary_line(wl, r, steps):
         "head_deviation": wl.structure.noise, "num_proxy_groups": wl.num_proxy_groups,
         "min_budget_tokens": wl.min_budget_tokens, "steps": steps,
         "ms_per_step": round(r["ms_total"], 4), "t_estimate_ms": round(r["t_est"], 4),
-        "t_select_ms": round(r["t_sel"], 4), "t_attention_ms": round(r["t_attn"], 4),
+        "t_select_ms": round(r["t_sel"], 4), "t_prepare_kv_ms": round(r["t_prep"], 4),
+        "t_attention_ms": round(r["t_attn"], 4),
         "t_dense_ms": round(r["t_dense"], 4) if r["t_dense"] else None,
         "speedup_vs_dense": round(r["t_dense"] / r["ms_total"], 3) if r["t_dense"] else None,
         "dense_equiv_tflops": round(r["f_dense"] / (r["ms_total"] * 1e-3) / 1e12, 2),
@@ -861,6 +879,7 @@ def main():
                    "min_budget_tokens": wl.min_budget_tokens, "parallelism": "single GPU"},
         "t_estimate_ms": round(t_est, 4),
         "t_select_ms": round(t_sel, 4),
+        "t_prepare_kv_ms": round(r["t_prep"], 4),
         "t_attention_ms": round(t_attn, 4),
         "step_ms_median": round(r["step_median"], 4) if r["step_median"] is not None else None,
         "step_ms_min": round(r["step_min"], 4) if r["step_min"] is not None else None,
@@ -871,6 +890,7 @@ def main():
         "estimation_overhead_pct": round(100.0 * (t_est + t_sel) / ms_total, 2),
         "sparsity": round(sparsity, 4),
         "t_dense_ms": round(t_dense, 4) if t_dense else None,
+        "t_dense_attention_ms": round(r["t_dense_attn"], 4) if t_dense else None,
         "speedup_vs_dense": round(t_dense / ms_total, 3) if t_dense else None,
         "estimation_overhead_pct_of_dense": round(100.0 * (t_est + t_sel) / t_dense, 2)
         if t_dense else None,
@@ -878,7 +898,7 @@ def main():
         "computed_blocks": total_blocks,
         "attention_mass_recall": ({k: round(x, 5) for k, x in r["recall"].items()}
                                   if r["recall"] else None),
-        "roofline": {"kernel": "attn_kernel (block-sparse prefill call)", "bound": "mfma",
+        "roofline": {"kernel": "attn_kernel (block-sparse blocked prefill call)", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic() if wl.name == "llama3_8b_n131072" and

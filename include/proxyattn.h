@@ -150,6 +150,9 @@ int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
  *      highest score down, then -1 up to Nk.  In this order the lists of the
  *      heads of one proxy group are prefixes of one another, which lets the
  *      attention step fetch shared key/value blocks once for all of them.
+ *      The same sets listed by ascending block index come from
+ *      proxyattn_budget followed by proxyattn_select_topk with mode
+ *      PROXYATTN_TOPK_CONSTANT | PROXYATTN_LIST_ASCENDING.
  */
 int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logscore,
                             const float* lastblk_mass, float gamma, int32_t min_budget_tokens,
@@ -167,18 +170,23 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
  *     (device array head_count [Hq] int32, in; values outside [0, Nk] are
  *     clamped to it), e.g. the output of proxyattn_budget, or one value for
  *     every head (the static Top-K allocation the paper compares against in
- *     its analysis of dynamic budgets, Sec. 5).  `mode` reads Eq. 3's
- *     K = b_i N (b_i = head_count[i] / Nk):
+ *     its analysis of dynamic budgets, Sec. 5).  `mode` is one reading of
+ *     Eq. 3's K = b_i N (b_i = head_count[i] / Nk), optionally OR-ed with
+ *     PROXYATTN_LIST_ASCENDING:
  *       PROXYATTN_TOPK_CONSTANT   N = Nk: every block row m keeps
  *                                 min(head_count[i], m+1) blocks (the reading
  *                                 proxyattn_select_budget uses);
  *       PROXYATTN_TOPK_ROW_RATIO  N = m+1, the row's causal blocks: row m
- *                                 keeps ceil(head_count[i] (m+1) / Nk) blocks.
- *     Outputs as for proxyattn_select_budget (lists from the highest score
- *     down, -1 padded).  Any other mode: PROXYATTN_E_INVALID.
+ *                                 keeps ceil(head_count[i] (m+1) / Nk) blocks;
+ *       PROXYATTN_LIST_ASCENDING  list each row's blocks by ascending block
+ *                                 index instead of from the highest score
+ *                                 down (the same set of blocks; -1 padded).
+ *     Other outputs as for proxyattn_select_budget.  Any other bit in mode:
+ *     PROXYATTN_E_INVALID.
  */
 #define PROXYATTN_TOPK_CONSTANT 0
 #define PROXYATTN_TOPK_ROW_RATIO 1
+#define PROXYATTN_LIST_ASCENDING 2
 
 int proxyattn_budget(const proxyattn_problem* p, const float* lastblk_mass, float gamma,
                      int32_t min_budget_tokens, int32_t* head_count, void* stream);
@@ -197,12 +205,52 @@ int proxyattn_select_topk(const proxyattn_problem* p, const float* block_logscor
  * out of bounds).  Blocks are accumulated in list order.
  *  out: [N][Hq][d] in the problem's dtype (o strides).
  *  lse: [Hq][N] fp32 natural-log row log-sum-exp, or NULL.
- *  workspace: as for proxyattn_estimate (holds a blocked copy of V).
+ *  workspace: as for proxyattn_estimate.  The call first copies K and V into
+ *      the blocked layout of proxyattn_prepare_kv inside the workspace, then
+ *      runs proxyattn_block_sparse_prefill_blocked on that copy.
  */
 int proxyattn_block_sparse_prefill(const proxyattn_problem* p, const void* q, const void* k,
                                    const void* v, const int32_t* block_count,
                                    const int32_t* block_index, void* out, float* lse,
                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The attention kernels read K and V from a blocked copy made once per K/V:
+ * for every KV head and key block, its keys and its values transposed, cut
+ * into sub-blocks of 64 keys that are each one contiguous chunk (rows past N
+ * are zero).  Callers that run several attention calls on the same K and V
+ * (the sparse path and its dense baseline, several thresholds) make the copy
+ * once with proxyattn_prepare_kv and pass it to the _blocked calls below.
+ * The layout is private to the library; only its size is part of the ABI.
+ *
+ * proxyattn_kv_blocked_size: bytes of the copy,
+ *     Hkv * ceil(N/b) * 2 * b * d * sizeof(element).
+ * proxyattn_prepare_kv: writes the copy of k and v (problem strides) to
+ *     kv_blocked (device, 16-byte aligned, at least proxyattn_kv_blocked_size
+ *     bytes, else PROXYATTN_E_WORKSPACE).
+ * proxyattn_blocked_workspace_size: bytes of workspace the _blocked calls
+ *     need (the attention kernel's work-queue counters; a small constant).
+ * proxyattn_block_sparse_prefill_blocked / proxyattn_dense_prefill_blocked:
+ *     as proxyattn_block_sparse_prefill / proxyattn_dense_prefill, reading K
+ *     and V from kv_blocked (written by proxyattn_prepare_kv for the same
+ *     problem; kv_blocked_bytes as above).  workspace: at least
+ *     proxyattn_blocked_workspace_size bytes; calls that share it must be
+ *     ordered.
+ */
+int proxyattn_kv_blocked_size(const proxyattn_problem* p, size_t* bytes);
+int proxyattn_prepare_kv(const proxyattn_problem* p, const void* k, const void* v,
+                         void* kv_blocked, size_t kv_blocked_bytes, void* stream);
+int proxyattn_blocked_workspace_size(const proxyattn_problem* p, size_t* bytes);
+int proxyattn_block_sparse_prefill_blocked(const proxyattn_problem* p, const void* q,
+                                           const void* kv_blocked, size_t kv_blocked_bytes,
+                                           const int32_t* block_count,
+                                           const int32_t* block_index, void* out, float* lse,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream);
+int proxyattn_dense_prefill_blocked(const proxyattn_problem* p, const void* q,
+                                    const void* kv_blocked, size_t kv_blocked_bytes, void* out,
+                                    float* lse, void* workspace, size_t workspace_bytes,
+                                    void* stream);
 
 /*
  * Checks caller-made lists against what proxyattn_block_sparse_prefill
@@ -223,7 +271,8 @@ int proxyattn_block_sparse_prefill(const proxyattn_problem* p, const void* q, co
 int proxyattn_check_lists(const proxyattn_problem* p, const int32_t* block_count,
                           const int32_t* block_index, int32_t* status, void* stream);
 
-/* Dense causal attention with the same kernels (every block n <= m). */
+/* Dense causal attention with the same kernels (every block n <= m); the
+ * workspace holds the blocked K/V copy as for the sparse call. */
 int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const void* k,
                             const void* v, void* out, float* lse, void* workspace,
                             size_t workspace_bytes, void* stream);

@@ -154,6 +154,11 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     return PROXYATTN_OK;
 }
 
+size_t kv_blocked_bytes(const Shape& sh) {
+    const size_t esz = sh.dtype == PROXYATTN_BF16 ? 2 : 4;
+    return (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz;
+}
+
 WsLayout ws_layout(const Shape& sh) {
     const size_t esz = sh.dtype == PROXYATTN_BF16 ? 2 : 4;
     WsLayout L{};
@@ -164,8 +169,8 @@ WsLayout ws_layout(const Shape& sh) {
     L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.b * sh.mq * 8);
     L.lnorm = off; off = align_up(off + (size_t)sh.hq * sh.b * 4);
-    L.kvb = off;  off = align_up(off + (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz);
-    L.queue = off; off = align_up(off + (size_t)kNumXcd * kQueueStride * 4);
+    L.kvb = off;  off = align_up(off + kv_blocked_bytes(sh));
+    L.queue = off; off = align_up(off + kQueueBytes);
     // the diagnostic reuses the re-blocked K/V region (never live at the same time)
     L.diag = L.kvb;
     const size_t diag_end = L.diag + align_up((size_t)sh.hq * sh.n * 4) + align_up((size_t)sh.hq * 8);
@@ -271,7 +276,7 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
     const int min_blocks = (int)(min_blocks64 > sh.mq ? sh.mq : min_blocks64);
     hipStream_t st = (hipStream_t)stream;
     PA_LAUNCH(launch_budget(sh, lastblk_mass, gamma, min_blocks, head_count, st), "budget");
-    PA_LAUNCH(launch_select(sh, block_logscore, head_count, 0, block_count, block_index, st),
+    PA_LAUNCH(launch_select(sh, block_logscore, head_count, 0, 0, block_count, block_index, st),
               "select");
     return PROXYATTN_OK;
 }
@@ -300,15 +305,16 @@ int proxyattn_select_topk(const proxyattn_problem* p, const float* block_logscor
     g_last_error[0] = 0;
     Shape sh;
     PA_TRY(resolve(p, &sh));
-    if (mode != PROXYATTN_TOPK_CONSTANT && mode != PROXYATTN_TOPK_ROW_RATIO)
+    if (mode & ~(PROXYATTN_TOPK_ROW_RATIO | PROXYATTN_LIST_ASCENDING))
         return fail(PROXYATTN_E_INVALID, "unknown top-k mode %d", (int)mode);
     if (sh.n == 0) return PROXYATTN_OK;
     PA_TRY(check_ptr(block_logscore, "block_logscore"));
     PA_TRY(check_ptr(head_count, "head_count"));
     PA_TRY(check_ptr(block_count, "block_count"));
     PA_TRY(check_ptr(block_index, "block_index"));
-    PA_LAUNCH(launch_select(sh, block_logscore, head_count, mode == PROXYATTN_TOPK_ROW_RATIO,
-                            block_count, block_index, (hipStream_t)stream),
+    PA_LAUNCH(launch_select(sh, block_logscore, head_count, (mode & PROXYATTN_TOPK_ROW_RATIO) != 0,
+                            (mode & PROXYATTN_LIST_ASCENDING) != 0, block_count, block_index,
+                            (hipStream_t)stream),
               "select");
     return PROXYATTN_OK;
 }
@@ -327,6 +333,26 @@ int proxyattn_check_lists(const proxyattn_problem* p, const int32_t* block_count
     return PROXYATTN_OK;
 }
 
+static int check_kvb(const Shape& sh, const void* kvb, size_t bytes) {
+    PA_TRY(check_ptr(kvb, "kv_blocked"));
+    const size_t need = kv_blocked_bytes(sh);
+    if (bytes < need)
+        return fail(PROXYATTN_E_WORKSPACE, "kv_blocked %zu bytes < %zu needed", bytes, need);
+    return PROXYATTN_OK;
+}
+
+static int check_attn_args(const Shape& sh, const void* q, const int32_t* block_count,
+                           const int32_t* block_index, void* out, float* lse, bool dense) {
+    PA_TRY(check_ptr(q, "q"));
+    PA_TRY(check_ptr(out, "out"));
+    if (!dense) {
+        PA_TRY(check_ptr(block_count, "block_count"));
+        PA_TRY(check_ptr(block_index, "block_index"));
+    }
+    if (lse && ((uintptr_t)lse & 3u)) return fail(PROXYATTN_E_INVALID, "lse not 4-byte aligned");
+    return PROXYATTN_OK;
+}
+
 static int prefill_common(const proxyattn_problem* p, const void* q, const void* k,
                           const void* v, const int32_t* block_count, const int32_t* block_index,
                           void* out, float* lse, void* workspace, size_t workspace_bytes,
@@ -335,23 +361,42 @@ static int prefill_common(const proxyattn_problem* p, const void* q, const void*
     Shape sh;
     PA_TRY(resolve(p, &sh));
     if (sh.n == 0) return PROXYATTN_OK;
-    PA_TRY(check_ptr(q, "q"));
     PA_TRY(check_ptr(k, "k"));
     PA_TRY(check_ptr(v, "v"));
-    PA_TRY(check_ptr(out, "out"));
-    if (!dense) {
-        PA_TRY(check_ptr(block_count, "block_count"));
-        PA_TRY(check_ptr(block_index, "block_index"));
-    }
-    if (lse && ((uintptr_t)lse & 3u)) return fail(PROXYATTN_E_INVALID, "lse not 4-byte aligned");
+    PA_TRY(check_attn_args(sh, q, block_count, block_index, out, lse, dense));
     WsLayout L;
     PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
     int* queue = (int*)(ws + L.queue);
+    // the re-blocking kernel also clears the work-queue counters
     PA_LAUNCH(launch_kv_block(sh, k, v, ws + L.kvb, queue, st), "kv_block");
     PA_LAUNCH(launch_attention(sh, dense, q, ws + L.kvb, block_count, block_index, out, lse, queue,
                                st),
+              "attention");
+    return PROXYATTN_OK;
+}
+
+static int prefill_blocked_common(const proxyattn_problem* p, const void* q, const void* kvb,
+                                  size_t kvb_bytes, const int32_t* block_count,
+                                  const int32_t* block_index, void* out, float* lse,
+                                  void* workspace, size_t workspace_bytes, void* stream,
+                                  bool dense) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_kvb(sh, kvb, kvb_bytes));
+    PA_TRY(check_attn_args(sh, q, block_count, block_index, out, lse, dense));
+    if (!workspace) return fail(PROXYATTN_E_INVALID, "workspace is NULL");
+    if (!aligned16(workspace)) return fail(PROXYATTN_E_INVALID, "workspace not 16-byte aligned");
+    if (workspace_bytes < kQueueBytes)
+        return fail(PROXYATTN_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes,
+                    kQueueBytes);
+    hipStream_t st = (hipStream_t)stream;
+    int* queue = (int*)workspace;
+    PA_LAUNCH(launch_queue_reset(queue, st), "queue_reset");
+    PA_LAUNCH(launch_attention(sh, dense, q, kvb, block_count, block_index, out, lse, queue, st),
               "attention");
     return PROXYATTN_OK;
 }
@@ -369,6 +414,55 @@ int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const voi
                             size_t workspace_bytes, void* stream) {
     return prefill_common(p, q, k, v, nullptr, nullptr, out, lse, workspace, workspace_bytes,
                           stream, true);
+}
+
+int proxyattn_kv_blocked_size(const proxyattn_problem* p, size_t* bytes) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (!bytes) return fail(PROXYATTN_E_INVALID, "bytes is NULL");
+    *bytes = kv_blocked_bytes(sh);
+    return PROXYATTN_OK;
+}
+
+int proxyattn_prepare_kv(const proxyattn_problem* p, const void* k, const void* v,
+                         void* kv_blocked, size_t kv_blocked_bytes_, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_ptr(k, "k"));
+    PA_TRY(check_ptr(v, "v"));
+    PA_TRY(check_kvb(sh, kv_blocked, kv_blocked_bytes_));
+    PA_LAUNCH(launch_kv_block(sh, k, v, kv_blocked, nullptr, (hipStream_t)stream), "kv_block");
+    return PROXYATTN_OK;
+}
+
+int proxyattn_blocked_workspace_size(const proxyattn_problem* p, size_t* bytes) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (!bytes) return fail(PROXYATTN_E_INVALID, "bytes is NULL");
+    *bytes = sh.n == 0 ? 0 : kQueueBytes;
+    return PROXYATTN_OK;
+}
+
+int proxyattn_block_sparse_prefill_blocked(const proxyattn_problem* p, const void* q,
+                                           const void* kv_blocked, size_t kv_blocked_bytes_,
+                                           const int32_t* block_count,
+                                           const int32_t* block_index, void* out, float* lse,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+    return prefill_blocked_common(p, q, kv_blocked, kv_blocked_bytes_, block_count, block_index,
+                                  out, lse, workspace, workspace_bytes, stream, false);
+}
+
+int proxyattn_dense_prefill_blocked(const proxyattn_problem* p, const void* q,
+                                    const void* kv_blocked, size_t kv_blocked_bytes_, void* out,
+                                    float* lse, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+    return prefill_blocked_common(p, q, kv_blocked, kv_blocked_bytes_, nullptr, nullptr, out, lse,
+                                  workspace, workspace_bytes, stream, true);
 }
 
 const char* proxyattn_error_string(int code) {

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) void kv_block_kernel(Shape sh, const T* __rest
                                                        T* __restrict__ kvb,
                                                        int* __restrict__ queue) {
     static_assert(kNumXcd * kQueueStride <= 256, "one thread per queue word");
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < kNumXcd * kQueueStride)
+    if (queue && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < kNumXcd * kQueueStride)
         queue[threadIdx.x] = 0;
     constexpr int V = Vec16<T>::n;
     constexpr int LDR = D + V;
@@ -99,6 +99,18 @@ __global__ __launch_bounds__(256) void kv_block_kernel(Shape sh, const T* __rest
         }
         *reinterpret_cast<u32x4*>(dst + sub * SUB + KT * D + d * KT + p0) = x;
     }
+}
+
+// Clears the attention work-queue counters (a fill kernel rather than a
+// memset, so that the sequence stays correct when a caller records it in a
+// graph).
+__global__ __launch_bounds__(256) void queue_reset_kernel(int* __restrict__ queue) {
+    if (threadIdx.x < kNumXcd * kQueueStride) queue[threadIdx.x] = 0;
+}
+
+hipError_t launch_queue_reset(int* queue, hipStream_t st) {
+    hipLaunchKernelGGL(queue_reset_kernel, dim3(1), dim3(256), 0, st, queue);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

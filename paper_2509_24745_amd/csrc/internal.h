@@ -47,6 +47,7 @@ constexpr size_t kMallBytes = (size_t)256 << 20;
 // The attention kernel is persistent: its workgroups pull work items from
 // kNumXcd queues (one int32 counter per queue, each on its own 128-byte line).
 constexpr int kQueueStride = 32;
+constexpr size_t kQueueBytes = (size_t)kNumXcd * kQueueStride * 4;
 
 // Largest key chunk of the last-block mass kernels (a multiple of every
 // block size); shorter sequences halve it down to one block.
@@ -78,6 +79,9 @@ struct WsLayout {
 
 WsLayout ws_layout(const Shape& sh);
 
+// Bytes of the blocked K/V copy: [Hkv][Mq][2 b d] elements.
+size_t kv_blocked_bytes(const Shape& sh);
+
 hipError_t launch_pool(const Shape& sh, const void* q, const void* k, void* qg, void* kg,
                        hipStream_t st);
 hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
@@ -89,13 +93,16 @@ hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* pa
 hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
-                         int row_ratio, int* block_count, int* block_index, hipStream_t st);
+                         int row_ratio, int ascending, int* block_count, int* block_index,
+                         hipStream_t st);
 hipError_t launch_check_lists(const Shape& sh, const int* block_count, const int* block_index,
                               int* status, hipStream_t st);
-// launch_kv_block also resets the attention work queues; launch_attention
-// must follow it on the same stream.
+// launch_kv_block also resets the attention work queues when `queue` is not
+// NULL; launch_queue_reset resets them alone.  Either must precede every
+// launch_attention on the same stream.
 hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,
                            hipStream_t st);
+hipError_t launch_queue_reset(int* queue, hipStream_t st);
 hipError_t launch_head_overlap(const Shape& sh, const void* q, const void* k, int t, int topk,
                                int sink, int renorm, float* z, uint64_t* kth, float* score,
                                hipStream_t st);

@@ -15,7 +15,9 @@
 //   Rank order makes the lists of a group's heads prefixes of one another,
 //   so the attention workgroups of those heads, which run side by side on
 //   one XCD, fetch the same K/V blocks in the same order; blocks read close
-//   together in time are shared through the L2.
+//   together in time are shared through the L2.  On request the same sets
+//   are listed by ascending block index instead (a rank table in LDS and a
+//   stream compaction per head).
 // check_lists: one workgroup per (block row m, head i); validates a
 //   caller-made list against what the attention step accepts.
 #include "common.h"
@@ -120,18 +122,20 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(Shape sh,
 }
 
 // ---------------------------------------------------------------------------
-// select: grid (Mq, G), 256 threads, dynamic LDS = P * 8 bytes
+// select: grid (Mq, G), 256 threads, dynamic LDS = P * 8 bytes (+ P * 4 for
+// ascending lists)
 // ---------------------------------------------------------------------------
 constexpr int kSelectThreads = 256;
 
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
                                                                 const float* __restrict__ logA,
                                                                 const int* __restrict__ head_count,
-                                                                int row_ratio,
+                                                                int row_ratio, int ascending,
                                                                 int* __restrict__ block_count,
                                                                 int* __restrict__ block_index) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-    const int tid = threadIdx.x;
+    __shared__ int wsum[kSelectThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int m = blockIdx.x, g = blockIdx.y, nk = sh.mq;
     const int ncand = m + 1;
     const int P = next_pow2(ncand);
@@ -145,17 +149,47 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     }
     __syncthreads();
     bitonic_sort_asc<uint64_t>(key, P, tid, kSelectThreads);
-    // the sorted keys are the candidates in rank order: a head's list is the
-    // first min(count, m+1) of them (lists of one group are prefixes of
-    // each other)
+    // ascending lists: rank[n] = position of block n in the rank order; each
+    // thread owns E consecutive candidates
+    int* rank = reinterpret_cast<int*>(key + P);
+    const int E = (ncand + kSelectThreads - 1) / kSelectThreads;
+    const int n0 = min(tid * E, ncand), n1 = min(n0 + E, ncand);
+    if (ascending) {
+        for (int p = tid; p < ncand; p += kSelectThreads) rank[(int)(key[p] & 0xffffffffu)] = p;
+        __syncthreads();
+    }
+    // the sorted keys are the candidates in rank order: a head's set is the
+    // first min(count, m+1) of them (sets of one group are prefixes of each
+    // other); it is listed in that order, or by ascending block index
     for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
         // counts outside [0, Nk] (caller-supplied) are clamped
         const int c = min(max(head_count[i], 0), nk);
         // per-row ratio: ceil(c (m+1) / Nk), exact in integers (< 2^26)
         const int kk = row_ratio ? min((c * ncand + nk - 1) / nk, ncand) : min(c, ncand);
         int* out = block_index + ((int64_t)i * sh.mq + m) * nk;
-        for (int p = tid; p < nk; p += kSelectThreads)
-            out[p] = p < kk ? (int)(key[p] & 0xffffffffu) : -1;
+        if (!ascending) {
+            for (int p = tid; p < nk; p += kSelectThreads)
+                out[p] = p < kk ? (int)(key[p] & 0xffffffffu) : -1;
+        } else {
+            // stream compaction of the blocks with rank < kk, in index order:
+            // a thread's own count, then an exclusive scan over the workgroup
+            int own = 0;
+            for (int n = n0; n < n1; ++n) own += rank[n] < kk;
+            int incl = own;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int y = __shfl_up(incl, o);
+                if (lane >= o) incl += y;
+            }
+            if (lane == 63) wsum[w] = incl;
+            __syncthreads();
+            int pos = incl - own;
+            for (int j = 0; j < w; ++j) pos += wsum[j];
+            for (int n = n0; n < n1; ++n)
+                if (rank[n] < kk) out[pos++] = n;
+            for (int p = kk + tid; p < nk; p += kSelectThreads) out[p] = -1;
+            __syncthreads();   // wsum is reused by the next head
+        }
         if (tid == 0) block_count[(int64_t)i * sh.mq + m] = kk;
     }
 }
@@ -210,15 +244,17 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
 }
 
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
-                         int row_ratio, int* block_count, int* block_index, hipStream_t st) {
-    const size_t smem = (size_t)next_pow2(sh.mq) * 8;
+                         int row_ratio, int ascending, int* block_count, int* block_index,
+                         hipStream_t st) {
+    const size_t P = (size_t)next_pow2(sh.mq);
+    const size_t smem = P * 8 + (ascending ? P * 4 : 0);
     if (smem > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(select_kernel, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh, logA,
-                       head_count, row_ratio, block_count, block_index);
+                       head_count, row_ratio, ascending, block_count, block_index);
     return hipGetLastError();
 }
 

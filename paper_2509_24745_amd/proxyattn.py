@@ -22,7 +22,7 @@ BF16 = 0
 F32 = 1
 
 E_OK, E_INVALID, E_UNSUPPORTED, E_WORKSPACE, E_HIP = 0, 1, 2, 3, 4
-TOPK_CONSTANT, TOPK_ROW_RATIO = 0, 1
+TOPK_CONSTANT, TOPK_ROW_RATIO, LIST_ASCENDING = 0, 1, 2
 LIST_BAD_COUNT, LIST_BAD_INDEX, LIST_DUPLICATE = 1, 2, 4
 
 
@@ -65,6 +65,14 @@ _SIGS = {
     "proxyattn_check_lists": [ctypes.c_void_p] * 5,
     "proxyattn_block_sparse_prefill": [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_dense_prefill": [ctypes.c_void_p] * 7 + [ctypes.c_size_t, ctypes.c_void_p],
+    "proxyattn_kv_blocked_size": [ctypes.c_void_p, ctypes.c_void_p],
+    "proxyattn_prepare_kv": [ctypes.c_void_p] * 4 + [ctypes.c_size_t, ctypes.c_void_p],
+    "proxyattn_blocked_workspace_size": [ctypes.c_void_p, ctypes.c_void_p],
+    "proxyattn_block_sparse_prefill_blocked": [ctypes.c_void_p] * 3 + [ctypes.c_size_t]
+                                              + [ctypes.c_void_p] * 5
+                                              + [ctypes.c_size_t, ctypes.c_void_p],
+    "proxyattn_dense_prefill_blocked": [ctypes.c_void_p] * 3 + [ctypes.c_size_t]
+                                       + [ctypes.c_void_p] * 3 + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_error_string": [ctypes.c_int],
     "proxyattn_last_error": [],
     "proxyattn_version": [],
@@ -181,6 +189,20 @@ def proxyattn_workspace_size(prob: Problem) -> int:
     n = ctypes.c_size_t(0)
     p = prob.c_struct()
     _check(lib().proxyattn_workspace_size(ctypes.byref(p), ctypes.byref(n)))
+    return n.value
+
+
+def proxyattn_kv_blocked_size(prob: Problem) -> int:
+    n = ctypes.c_size_t(0)
+    p = prob.c_struct()
+    _check(lib().proxyattn_kv_blocked_size(ctypes.byref(p), ctypes.byref(n)))
+    return n.value
+
+
+def proxyattn_blocked_workspace_size(prob: Problem) -> int:
+    n = ctypes.c_size_t(0)
+    p = prob.c_struct()
+    _check(lib().proxyattn_blocked_workspace_size(ctypes.byref(p), ctypes.byref(n)))
     return n.value
 
 
@@ -355,6 +377,52 @@ def proxyattn_dense_prefill(prob: Problem, q, k, v, out, lse, workspace, stream=
     _check(lib().proxyattn_dense_prefill(
         ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(workspace),
         _nbytes(workspace) if workspace is not None else 0, _stream(stream)))
+
+
+def _need_kvb(prob: Problem, kv_blocked):
+    if kv_blocked is None or isinstance(kv_blocked, int):
+        return
+    _need_ws(kv_blocked, proxyattn_kv_blocked_size(prob), "kv_blocked")
+
+
+def proxyattn_prepare_kv(prob: Problem, k, v, kv_blocked, stream=None):
+    _need_kv(prob, k, "k")
+    _need_kv(prob, v, "v")
+    _need_kvb(prob, kv_blocked)
+    p = prob.c_struct()
+    _check(lib().proxyattn_prepare_kv(ctypes.byref(p), _ptr(k), _ptr(v), _ptr(kv_blocked),
+                                      _nbytes(kv_blocked) if kv_blocked is not None else 0,
+                                      _stream(stream)))
+
+
+def proxyattn_block_sparse_prefill_blocked(prob: Problem, q, kv_blocked, block_count, block_index,
+                                           out, lse, workspace, stream=None):
+    _need_q(prob, q)
+    _need_kvb(prob, kv_blocked)
+    _need_lists(prob, block_count, block_index)
+    _need_out(prob, out)
+    _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
+    _need_ws(workspace, 0)
+    p = prob.c_struct()
+    _check(lib().proxyattn_block_sparse_prefill_blocked(
+        ctypes.byref(p), _ptr(q), _ptr(kv_blocked),
+        _nbytes(kv_blocked) if kv_blocked is not None else 0, _ptr(block_count),
+        _ptr(block_index), _ptr(out), _ptr(lse), _ptr(workspace),
+        _nbytes(workspace) if workspace is not None else 0, _stream(stream)))
+
+
+def proxyattn_dense_prefill_blocked(prob: Problem, q, kv_blocked, out, lse, workspace,
+                                    stream=None):
+    _need_q(prob, q)
+    _need_kvb(prob, kv_blocked)
+    _need_out(prob, out)
+    _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
+    _need_ws(workspace, 0)
+    p = prob.c_struct()
+    _check(lib().proxyattn_dense_prefill_blocked(
+        ctypes.byref(p), _ptr(q), _ptr(kv_blocked),
+        _nbytes(kv_blocked) if kv_blocked is not None else 0, _ptr(out), _ptr(lse),
+        _ptr(workspace), _nbytes(workspace) if workspace is not None else 0, _stream(stream)))
 
 
 def proxyattn_version() -> str:

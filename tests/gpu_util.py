@@ -80,6 +80,19 @@ def run_attention(prob: pa.Problem, q, k, v, block_count=None, block_index=None,
     return to_host(bufs.out), to_host(bufs.lse)
 
 
+_INPUTS: dict = {}
+
+
 def inputs(wl: Workload):
-    g = generate(wl)
-    return g["q"], g["k"], g["v"]
+    """Seeded inputs of `wl`.  The draw depends on the shape, block size,
+    dtype, seed and structure only (not on G, stride, gamma or the minimum
+    budget); the last two draws stay cached, since the large layers are
+    shared by several tests and take tens of seconds to draw."""
+    key = (wl.seq_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.block_size, wl.dtype,
+           wl.seed, wl.structure)
+    if key not in _INPUTS:
+        while len(_INPUTS) >= 2:
+            _INPUTS.pop(next(iter(_INPUTS)))
+        g = generate(wl)
+        _INPUTS[key] = (g["q"], g["k"], g["v"])
+    return _INPUTS[key]

@@ -204,7 +204,7 @@ def test_calls_reject_bad_arguments_before_launch():
     assert lib.proxyattn_check_lists(ctypes.byref(p), None, fake, fake, None) == pa.E_INVALID
     assert lib.proxyattn_check_lists(ctypes.byref(p), fake, fake + 4, fake, None) == pa.E_INVALID
     # unknown top-k mode, missing counts
-    for mode in (-1, 2, 7):
+    for mode in (-1, 4, 7):
         assert lib.proxyattn_select_topk(ctypes.byref(p), fake, fake, mode, fake, fake, None) \
             == pa.E_INVALID
     assert b"mode" in lib.proxyattn_last_error()
@@ -223,6 +223,26 @@ def test_calls_reject_bad_arguments_before_launch():
     # prefill without lists
     assert lib.proxyattn_block_sparse_prefill(ctypes.byref(p), fake, fake, fake, None, fake, fake,
                                               None, fake, ws, None) == pa.E_INVALID
+    # blocked K/V copy: missing, misaligned, too small; blocked calls' workspace
+    kvb = pa.proxyattn_kv_blocked_size(prob)
+    qws = pa.proxyattn_blocked_workspace_size(prob)
+    assert lib.proxyattn_prepare_kv(ctypes.byref(p), fake, fake, None, kvb, None) == pa.E_INVALID
+    assert lib.proxyattn_prepare_kv(ctypes.byref(p), fake, fake, fake + 8, kvb, None) \
+        == pa.E_INVALID
+    assert lib.proxyattn_prepare_kv(ctypes.byref(p), fake, fake, fake, kvb - 1, None) \
+        == pa.E_WORKSPACE
+    assert lib.proxyattn_prepare_kv(ctypes.byref(p), None, fake, fake, kvb, None) == pa.E_INVALID
+    assert lib.proxyattn_block_sparse_prefill_blocked(ctypes.byref(p), fake, fake, kvb - 1, fake,
+                                                      fake, fake, None, fake, qws, None) \
+        == pa.E_WORKSPACE
+    assert lib.proxyattn_block_sparse_prefill_blocked(ctypes.byref(p), fake, fake, kvb, fake,
+                                                      fake, fake, None, fake, qws - 1, None) \
+        == pa.E_WORKSPACE
+    assert lib.proxyattn_block_sparse_prefill_blocked(ctypes.byref(p), fake, fake, kvb, None,
+                                                      fake, fake, None, fake, qws, None) \
+        == pa.E_INVALID
+    assert lib.proxyattn_dense_prefill_blocked(ctypes.byref(p), fake, fake, kvb, fake, None, None,
+                                               qws, None) == pa.E_INVALID
     # empty problem: valid no-op, nothing touched
     p0 = _prob(seq_len=0).c_struct()
     assert lib.proxyattn_estimate(ctypes.byref(p0), None, None, None, None, None, 0, None) == 0
@@ -231,6 +251,25 @@ def test_calls_reject_bad_arguments_before_launch():
                                      None) == 0
     assert lib.proxyattn_dense_prefill(ctypes.byref(p0), None, None, None, None, None, None, 0,
                                        None) == 0
+    assert lib.proxyattn_prepare_kv(ctypes.byref(p0), None, None, None, 0, None) == 0
+    assert lib.proxyattn_dense_prefill_blocked(ctypes.byref(p0), None, None, 0, None, None, None,
+                                               0, None) == 0
+
+
+@pytest.mark.parametrize("n,hkv,d,b,dtype,esz", [(131072, 8, 128, 128, "bf16", 2),
+                                                  (2048, 2, 64, 64, "fp32", 4),
+                                                  (1000, 8, 128, 128, "bf16", 2)])
+def test_blocked_sizes(n, hkv, d, b, dtype, esz):
+    """The blocked K/V copy holds every KV head's keys and values in whole
+    blocks (the ragged last block padded); the blocked calls' workspace is
+    the kernel's eight 128-byte work-queue lines."""
+    _lib()
+    prob = _prob(seq_len=n, num_kv_heads=hkv, num_q_heads=4 * hkv, num_proxy_groups=hkv,
+                 head_dim=d, block_size=b, dtype=dtype)
+    assert pa.proxyattn_kv_blocked_size(prob) == hkv * -(-n // b) * 2 * b * d * esz
+    assert pa.proxyattn_blocked_workspace_size(prob) == 8 * 128
+    assert pa.proxyattn_kv_blocked_size(_prob(seq_len=0)) == 0
+    assert pa.proxyattn_blocked_workspace_size(_prob(seq_len=0)) == 0
 
 
 def test_binding_rejects_tensors_smaller_than_the_problem():

@@ -649,13 +649,15 @@ def _sampled_rows_check(wl, nsample: int):
           f"rows={rep.ambiguous_rows} of {rep.rows_checked}", flush=True)
 
 
-@pytest.mark.parametrize("layer", [0, 31])
+@pytest.mark.parametrize("layer", [0, 7, 15, 23, 31])
 def test_256k_layer_sampled_rows(layer):
-    """The first and the last layer of the 256K stack (layer l is drawn with
-    seed l), 32 sampled query rows each."""
+    """Five layers spread over the 32-layer 256K stack (layer l is drawn with
+    seed l): every head's last-block mass and budget, and the scores, lists
+    and attention of 512 sampled query rows per head (the same rows for every
+    head) and of their block rows."""
     wl = WORKLOADS["llama3_8b_n262144"].replace(seed=layer)
     print(f"\n[256K layer {layer}]", flush=True)
-    _sampled_rows_check(wl, 32)
+    _sampled_rows_check(wl, 512)
 
 
 def test_maximum_size_sampled_rows():
@@ -667,26 +669,80 @@ def test_maximum_size_sampled_rows():
     _sampled_rows_check(wl, 16)
 
 
-@pytest.mark.parametrize("name,kw,rows_per_head", [
-    ("llama3_8b_n32768", {}, 256),
-    ("llama3_8b_n131072", {}, 64),
-    # heterogeneous heads (half near-dense, half local + sink), 7 proxy groups
-    # of 4 query heads that straddle the 4 KV heads of 7, and a 2048-token
-    # minimum budget
-    ("qwen25_7b_n65536", {"num_proxy_groups": 7, "min_budget_tokens": 2048}, 128),
-], ids=["llama_n32768", "llama_n131072", "qwen_n65536_g7_beta2048"])
-def test_full_size_lists_and_sampled_attention(name, kw, rows_per_head):
-    """Full-size layers in the launch configuration the benchmark times: every
-    score, budget and list checked; attention on sampled query rows (seeded,
-    always including the last row)."""
+# The full-size 32K, 64K and 128K layers are checked in test_gpu_scope.py.
+
+
+@pytest.mark.parametrize("case", ["llama_n4173_ragged", "qwen_g7_n8192", "gqa8x2_n2048_fp32"])
+def test_ascending_lists_match_oracle(case):
+    """PROXYATTN_LIST_ASCENDING: the same sets as the rank-order lists, listed
+    by ascending block index, which is the oracle's own list order (Eq. 3);
+    where no threshold ambiguity arises the lists equal the oracle's bit for
+    bit.  Constant and per-row-ratio readings; attention on the ascending
+    lists against the oracle."""
     U = _gpu()
-    wl = WORKLOADS[name].replace(**kw) if kw else WORKLOADS[name]
-    print(f"\n[full size] {wl}", flush=True)
+    from paper_2509_24745_amd import proxyattn as pa
+    wl = CASES[case]
     q, k, v = U.inputs(wl)
     prob = U.problem_of(wl)
-    rng = np.random.default_rng(12345)
-    rows = np.unique(np.concatenate([rng.integers(0, wl.seq_len, rows_per_head),
-                                     [wl.seq_len - 1]]))
-    gpu = U.run_path(prob, q, k, v, wl.gamma, wl.min_budget_tokens)
+    qd, kd, vd = U.to_dev(q, prob), U.to_dev(k, prob), U.to_dev(v, prob)
+    bufs = pa.Buffers(prob)
+    pa.proxyattn_estimate(prob, qd, kd, bufs.logscore, bufs.mass, bufs.workspace)
+    pa.proxyattn_budget(prob, bufs.mass, wl.gamma, 0, bufs.head_count)
+    torch.cuda.synchronize()
+    counts = U.to_host(bufs.head_count)
     orc = _oracle(wl, q, k)
-    _compare(wl, q, k, v, gpu, orc, attn_rows=rows)
+    for row_ratio in (False, True):
+        mode = (pa.TOPK_ROW_RATIO if row_ratio else pa.TOPK_CONSTANT) | pa.LIST_ASCENDING
+        pa.proxyattn_select_topk(prob, bufs.logscore, bufs.head_count, mode, bufs.block_count,
+                                 bufs.block_index)
+        torch.cuda.synchronize()
+        bc, bi = U.to_host(bufs.block_count), U.to_host(bufs.block_index)
+        for i in range(wl.num_q_heads):
+            for m in range(prob.num_blocks):
+                c = int(bc[i, m])
+                assert np.all(np.diff(bi[i, m, :c]) > 0), (i, m, bi[i, m, :c])
+        rep = C.check_lists(bc, bi, orc["logA"], counts, wl.num_q_heads, rank_order=False,
+                            row_ratio=row_ratio)
+        obc, obi = O.select_blocks(orc["logA"], counts, wl.num_q_heads, row_ratio=row_ratio)
+        if rep.ambiguous_rows == 0:
+            assert np.array_equal(bc, obc) and np.array_equal(bi, obi)
+        out, lse = U.run_attention(prob, q, k, v, bc, bi)
+        ref, ref_lse = O.block_sparse_attention(q, k, v, bc, bi, wl.block_size,
+                                                O.default_scale(wl.head_dim))
+        arep = C.check_attention(out, ref)
+        assert float(np.max(np.abs(lse - ref_lse))) <= LSE_TOL
+        print(f"\n[ascending {case} row_ratio={row_ratio}] ambiguous rows {rep.ambiguous_rows} "
+              f"of {rep.rows_checked}; max|dO|={arep.max_abs:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("case", ["llama_n4173_ragged", "gqa8x2_n2048_fp32",
+                                  "bf16_d64_b64_s2_n3000", "fp32_d128_b64_n700",
+                                  "bf16_d128_b64_s4_n3100"])
+def test_blocked_calls_match_unblocked(case):
+    """proxyattn_prepare_kv once, then the _blocked sparse and dense calls
+    (twice each, sharing one small workspace, so the work-queue counters are
+    reset between launches): output and lse bitwise those of the calls that
+    re-block K/V themselves."""
+    U = _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    wl = CASES[case]
+    q, k, v = U.inputs(wl)
+    prob = U.problem_of(wl)
+    qd, kd, vd = U.to_dev(q, prob), U.to_dev(k, prob), U.to_dev(v, prob)
+    b = pa.prefill(prob, qd, kd, vd, wl.gamma)
+    dense_out, dense_lse = torch.empty_like(b.out), torch.empty_like(b.lse)
+    pa.proxyattn_dense_prefill(prob, qd, kd, vd, dense_out, dense_lse, b.workspace)
+    kvb = torch.empty(pa.proxyattn_kv_blocked_size(prob), dtype=torch.uint8, device="cuda")
+    qws = torch.empty(pa.proxyattn_blocked_workspace_size(prob), dtype=torch.uint8, device="cuda")
+    pa.proxyattn_prepare_kv(prob, kd, vd, kvb)
+    for rep in range(2):
+        out, lse = torch.full_like(b.out, float("nan")), torch.full_like(b.lse, float("nan"))
+        pa.proxyattn_block_sparse_prefill_blocked(prob, qd, kvb, b.block_count, b.block_index,
+                                                  out, lse, qws)
+        torch.cuda.synchronize()
+        assert torch.equal(out, b.out) and torch.equal(lse, b.lse), f"sparse, call {rep}"
+        out.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        pa.proxyattn_dense_prefill_blocked(prob, qd, kvb, out, lse, qws)
+        torch.cuda.synchronize()
+        assert torch.equal(out, dense_out) and torch.equal(lse, dense_lse), f"dense, call {rep}"
