@@ -16,7 +16,9 @@ from dataclasses import dataclass
 import torch  # loaded first: the library then binds to torch's HIP runtime
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libproxyattn.so")
+# PROXYATTN_LIBRARY selects another build of the library (the sanitized host
+# build for the boundary tests); by default the one next to this file
+LIB_PATH = os.environ.get("PROXYATTN_LIBRARY") or os.path.join(_HERE, "libproxyattn.so")
 
 BF16 = 0
 F32 = 1
