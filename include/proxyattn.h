@@ -103,6 +103,19 @@ typedef struct proxyattn_problem {
  * Bytes of device workspace that proxyattn_estimate and the two prefill
  * entry points need (the largest of their needs; one buffer serves all).
  * Returns PROXYATTN_OK and writes *bytes, or an error for a bad problem.
+ *
+ * The regions (each rounded up to 256 bytes; esz = element size, b' = b/s,
+ * C = key chunks of the block scoring, at most ceil(N'/4096)):
+ *   pooled Q^g and K^g      2 * G * N' * d * esz
+ *   row (max, sum) pairs    G * C * N' * 8
+ *   per-(row, block) maxima G * Mq(Mq+1)/2 * b' * 4
+ *   last-block pairs        Hq * b * Mq * 8, plus Hq * b * 4
+ *   blocked K/V copy        Hkv * Mq * 2 * b * d * esz
+ *   work-queue counters     1024
+ * The per-(row, block) maxima grow with the square of the sequence length:
+ * 268 MB at N = 131072 with G = 4, b' = 32; 4.3 GB per proxy group at the
+ * largest accepted size (Mq = 8192, b' = 32), 17 GB per group with s = 1 and
+ * b = 128.  A caller that cannot provide that much must shorten the problem.
  */
 int proxyattn_workspace_size(const proxyattn_problem* p, size_t* bytes);
 

@@ -171,6 +171,24 @@ def test_workspace_size_formula(n, hq, hkv, g, b, s):
     assert pa.proxyattn_workspace_size(prob) == max(end, diag_end)
 
 
+def test_workspace_size_at_the_largest_problem():
+    """8192 blocks: the per-(row, block) maxima dominate (G * Mq(Mq+1)/2 * b'
+    floats), 4.3 GB per proxy group with b' = 32 and 17 GB with s = 1."""
+    _lib()
+    mq = 8192
+    for g, s, bp in ((1, 4, 32), (4, 4, 32), (1, 1, 128)):
+        prob = _prob(seq_len=mq * 128, num_q_heads=32, num_kv_heads=8, num_proxy_groups=g,
+                     stride=s)
+        ws = pa.proxyattn_workspace_size(prob)
+        rbm = g * (mq * (mq + 1) // 2) * bp * 4
+        assert ws > rbm
+        assert ws < rbm + 4 * 2**30 * g + 3 * 2**30     # the other regions are a few GB
+        if (g, s) == (1, 4):
+            assert 4.2e9 < rbm < 4.4e9
+        if s == 1:
+            assert 17e9 < rbm < 17.3e9
+
+
 def test_workspace_size_of_empty_problem():
     _lib()
     assert pa.proxyattn_workspace_size(_prob(seq_len=0)) == 0
