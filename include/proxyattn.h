@@ -266,6 +266,28 @@ int proxyattn_dense_prefill_blocked(const proxyattn_problem* p, const void* q,
                                     void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * block-sparse attention of proxyattn_block_sparse_prefill_blocked with no
+ * workspace argument.  Arguments as there; results bitwise the same.  Its
+ * only scratch, the attention kernel's work-queue counters (1 KiB, whatever
+ * the problem size), lives in a static device array of 1 KiB that the
+ * library holds on every GPU it runs on until the process ends; a need
+ * beyond that size would fail with PROXYATTN_E_UNSUPPORTED.  The call
+ * allocates and frees nothing; its first call on a device looks the array's
+ * address up (a failure there returns PROXYATTN_E_HIP).  Every call on one
+ * GPU shares that GPU's array and clears it before use: calls that overlap
+ * on one GPU (concurrent streams, or threads without ordering) race and give
+ * wrong results; calls ordered on one stream are safe.
+ */
+int proxyattn_block_sparse_prefill_blocked_noalloc(const proxyattn_problem* p, const void* q,
+                                                   const void* kv_blocked,
+                                                   size_t kv_blocked_bytes,
+                                                   const int32_t* block_count,
+                                                   const int32_t* block_index, void* out,
+                                                   float* lse, void* stream);
+
+/*
  * Checks caller-made lists against what proxyattn_block_sparse_prefill
  * accepts: the lists of Eq. 3 (Sec. 3.2) select distinct causal key blocks
  * n <= m of query block m.  For every head i and block row m writes

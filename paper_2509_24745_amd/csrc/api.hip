@@ -416,6 +416,33 @@ int proxyattn_dense_prefill(const proxyattn_problem* p, const void* q, const voi
                           stream, true);
 }
 
+int proxyattn_block_sparse_prefill_blocked_noalloc(const proxyattn_problem* p, const void* q,
+                                                   const void* kv_blocked,
+                                                   size_t kv_blocked_bytes_,
+                                                   const int32_t* block_count,
+                                                   const int32_t* block_index, void* out,
+                                                   float* lse, void* stream) {
+    g_last_error[0] = 0;
+    Shape sh;
+    PA_TRY(resolve(p, &sh));
+    if (sh.n == 0) return PROXYATTN_OK;
+    PA_TRY(check_kvb(sh, kv_blocked, kv_blocked_bytes_));
+    PA_TRY(check_attn_args(sh, q, block_count, block_index, out, lse, false));
+    // the scratch this call needs (the work-queue counters) against the
+    // static array's size; the queues do not grow with the problem
+    if (kQueueBytes > kScratchBytes)
+        return fail(PROXYATTN_E_UNSUPPORTED, "scratch of %zu bytes needed, %zu available",
+                    kQueueBytes, kScratchBytes);
+    int* queue = nullptr;
+    PA_LAUNCH(scratch_address(&queue), "scratch address");
+    hipStream_t st = (hipStream_t)stream;
+    PA_LAUNCH(launch_queue_reset(queue, st), "queue_reset");
+    PA_LAUNCH(launch_attention(sh, false, q, kv_blocked, block_count, block_index, out, lse, queue,
+                               st),
+              "attention");
+    return PROXYATTN_OK;
+}
+
 int proxyattn_kv_blocked_size(const proxyattn_problem* p, size_t* bytes) {
     g_last_error[0] = 0;
     Shape sh;

@@ -113,6 +113,36 @@ hipError_t launch_queue_reset(int* queue, hipStream_t st) {
     return hipGetLastError();
 }
 
+// Scratch of the entry point that allocates nothing: the work-queue counters
+// live in this file-scope device array, one copy per GPU, for the life of
+// the process.  Host code never passes the array's name to a kernel (on the
+// host it is only a stand-in for the symbol); it uses the device address
+// that hipGetSymbolAddress returns, looked up once per device with that
+// device current and kept in scratch_ptr[].
+static __device__ __align__(256) int scratch[kScratchBytes / sizeof(int)];
+static_assert(kQueueBytes <= kScratchBytes, "the work queues fit the scratch array");
+
+constexpr int kMaxDevices = 64;
+static std::mutex scratch_mu;
+static int* scratch_ptr[kMaxDevices];
+
+hipError_t scratch_address(int** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        scratch_ptr[dev] = (int*)p;
+    }
+    *out = scratch_ptr[dev];
+    return hipSuccess;
+}
+
 // ---------------------------------------------------------------------------
 // attention.  Persistent grid (one workgroup per resident slot), 2B threads (B/32
 // waves), 2 workgroups per CU.

@@ -49,6 +49,10 @@ constexpr size_t kMallBytes = (size_t)256 << 20;
 constexpr int kQueueStride = 32;
 constexpr size_t kQueueBytes = (size_t)kNumXcd * kQueueStride * 4;
 
+// Size of the static device scratch array that the entry point which
+// allocates nothing uses instead of a workspace (it holds the work queues).
+constexpr size_t kScratchBytes = 1024;
+
 // Largest key chunk of the last-block mass kernels (a multiple of every
 // block size); shorter sequences halve it down to one block.
 constexpr int kMassChunk = 2048;
@@ -103,6 +107,9 @@ hipError_t launch_check_lists(const Shape& sh, const int* block_count, const int
 hipError_t launch_kv_block(const Shape& sh, const void* k, const void* v, void* kvb, int* queue,
                            hipStream_t st);
 hipError_t launch_queue_reset(int* queue, hipStream_t st);
+// Device address of the current device's static scratch array (looked up on
+// the first call per device).
+hipError_t scratch_address(int** out);
 hipError_t launch_head_overlap(const Shape& sh, const void* q, const void* k, int t, int topk,
                                int sink, int renorm, float* z, uint64_t* kth, float* score,
                                hipStream_t st);

@@ -75,6 +75,8 @@ _SIGS = {
                                               + [ctypes.c_size_t, ctypes.c_void_p],
     "proxyattn_dense_prefill_blocked": [ctypes.c_void_p] * 3 + [ctypes.c_size_t]
                                        + [ctypes.c_void_p] * 3 + [ctypes.c_size_t, ctypes.c_void_p],
+    "proxyattn_block_sparse_prefill_blocked_noalloc": [ctypes.c_void_p] * 3 + [ctypes.c_size_t]
+                                                      + [ctypes.c_void_p] * 5,
     "proxyattn_error_string": [ctypes.c_int],
     "proxyattn_last_error": [],
     "proxyattn_version": [],
@@ -411,6 +413,20 @@ def proxyattn_block_sparse_prefill_blocked(prob: Problem, q, kv_blocked, block_c
         _nbytes(kv_blocked) if kv_blocked is not None else 0, _ptr(block_count),
         _ptr(block_index), _ptr(out), _ptr(lse), _ptr(workspace),
         _nbytes(workspace) if workspace is not None else 0, _stream(stream)))
+
+
+def proxyattn_block_sparse_prefill_blocked_noalloc(prob: Problem, q, kv_blocked, block_count,
+                                                   block_index, out, lse, stream=None):
+    _need_q(prob, q)
+    _need_kvb(prob, kv_blocked)
+    _need_lists(prob, block_count, block_index)
+    _need_out(prob, out)
+    _need(lse, prob.num_q_heads * prob.seq_len, "lse", torch.float32)
+    p = prob.c_struct()
+    _check(lib().proxyattn_block_sparse_prefill_blocked_noalloc(
+        ctypes.byref(p), _ptr(q), _ptr(kv_blocked),
+        _nbytes(kv_blocked) if kv_blocked is not None else 0, _ptr(block_count),
+        _ptr(block_index), _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def proxyattn_dense_prefill_blocked(prob: Problem, q, kv_blocked, out, lse, workspace,
