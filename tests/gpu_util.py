@@ -36,11 +36,13 @@ def pooled_from_workspace(prob: pa.Problem, ws: torch.Tensor):
     return view(qo), view(ko)
 
 
-def run_path(prob: pa.Problem, q, k, v, gamma: float, min_budget: int = 0, lists=None):
+def run_path(prob: pa.Problem, q, k, v, gamma: float, min_budget: int = 0, lists=None,
+             rows=None):
     """Run estimate -> select_budget -> block_sparse_prefill; return numpy results.
 
     `lists`: optional (block_count, block_index) numpy arrays to feed the
-    attention instead of the selected lists.
+    attention instead of the selected lists.  `rows`: optional token indices;
+    only those rows of out and lse are fetched (out[rows], lse[:, rows]).
     """
     qd, kd = to_dev(q, prob), to_dev(k, prob)
     vd = to_dev(v, prob) if v is not None else None
@@ -63,7 +65,11 @@ def run_path(prob: pa.Problem, q, k, v, gamma: float, min_budget: int = 0, lists
                counts=to_host(bufs.head_count), block_count=to_host(bufs.block_count),
                block_index=to_host(bufs.block_index))
     if vd is not None:
-        res.update(out=to_host(bufs.out), lse=to_host(bufs.lse))
+        if rows is None:
+            res.update(out=to_host(bufs.out), lse=to_host(bufs.lse))
+        else:
+            r = torch.from_numpy(np.asarray(rows, dtype=np.int64)).cuda()
+            res.update(out=to_host(bufs.out[r]), lse=to_host(bufs.lse[:, r]))
     return res
 
 

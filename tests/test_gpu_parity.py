@@ -609,29 +609,36 @@ def test_whole_step_replays_from_a_hip_graph():
             assert torch.equal(getattr(bufs, n), ref[n]), f"replay {rep}: {n} differs"
 
 
-def _sampled_rows_check(wl, nsample: int):
+def _sampled_rows_check(wl, nsample: int, pre: dict | None = None):
     """The whole path at full size, in the benchmark's launch configuration:
     pooled heads bit-exact, every head's last-block mass and budget, and the
     proxy scores, lists and attention of seeded sampled query rows (always
-    including the last row) and their block rows."""
+    including the last row) and their block rows.  `pre`: the layer's inputs
+    and the oracle's pooled heads, block scores of those block rows and
+    masses, prepared ahead (tests/pregen.py); computed here when absent."""
     U = _gpu()
-    q, k, v = U.inputs(wl)
-    prob = U.problem_of(wl)
-    rng = np.random.default_rng(12345)
-    rows = np.unique(np.concatenate([rng.integers(0, wl.seq_len, nsample), [wl.seq_len - 1]]))
+    from tests import pregen
+    rows = pregen.sample_rows(wl.seq_len, nsample)
     brows = np.unique(rows // wl.block_size)
-    gpu = U.run_path(prob, q, k, v, wl.gamma)
     sc = O.default_scale(wl.head_dim)
-    qg, kg = O.pool_proxy_heads(q, k, wl.num_proxy_groups, wl.stride, wl.dtype)
+    if pre is None:
+        q, k, v = U.inputs(wl)
+        qg, kg = O.pool_proxy_heads(q, k, wl.num_proxy_groups, wl.stride, wl.dtype)
+        oa, _ = O.proxy_block_logscore(qg, kg, wl.seq_len, wl.block_size, wl.stride, sc,
+                                       rows=brows)
+        mass = O.lastblock_mass(q, k, wl.block_size, sc)
+    else:
+        q, k, v = pre["q"], pre["k"], pre["v"]
+        qg, kg, oa, mass = pre["qg"], pre["kg"], pre["logA"], pre["mass"]
+    prob = U.problem_of(wl)
+    gpu = U.run_path(prob, q, k, v, wl.gamma, rows=rows)
     assert np.array_equal(gpu["qg"], qg) and np.array_equal(gpu["kg"], kg), "pooled heads differ"
-    oa, _ = O.proxy_block_logscore(qg, kg, wl.seq_len, wl.block_size, wl.stride, sc, rows=brows)
     ga = gpu["logA"][:, brows]
     ob = oa[:, brows]
     assert np.array_equal(np.isneginf(ga), np.isneginf(ob)), "-inf pattern differs"
     fin = np.isfinite(ob)
     dla = float(np.max(np.abs(ga[fin] - ob[fin])))
     assert dla <= LOGA_TOL, f"max |dlogA| = {dla}"
-    mass = O.lastblock_mass(q, k, wl.block_size, sc)
     dm = float(np.max(np.abs(gpu["mass"] - mass))) / wl.block_size
     assert dm <= MASS_RTOL, f"max |dmass|/rows = {dm}"
     counts, cums = O.budget_counts(mass, wl.gamma, wl.min_budget_tokens, wl.block_size)
@@ -641,12 +648,13 @@ def _sampled_rows_check(wl, nsample: int):
                   rows=brows, report=rep)
     ref_out, ref_lse = O.block_sparse_attention(q, k, v, gpu["block_count"], gpu["block_index"],
                                                 wl.block_size, sc, query_rows=rows)
-    C.check_attention(gpu["out"][rows], ref_out[rows], rep)
-    dl = float(np.abs(gpu["lse"][:, rows] - ref_lse[:, rows]).max())
+    C.check_attention(gpu["out"], ref_out[rows], rep)
+    dl = float(np.abs(gpu["lse"] - ref_lse[:, rows]).max())
     assert dl <= LSE_TOL, f"max |dlse| = {dl}"
-    print(f"\n[{wl.name}] |dlogA|={dla:.2e} |dmass|/rows={dm:.2e} max|dO|={rep.max_abs:.2e} "
-          f"mean|dO|={rep.mean_abs:.2e} |dlse|={dl:.2e} ambiguous heads={len(rep.ambiguous_heads)} "
-          f"rows={rep.ambiguous_rows} of {rep.rows_checked}", flush=True)
+    print(f"\n[{wl.name} seed {wl.seed}] |dlogA|={dla:.2e} |dmass|/rows={dm:.2e} "
+          f"max|dO|={rep.max_abs:.2e} mean|dO|={rep.mean_abs:.2e} |dlse|={dl:.2e} "
+          f"ambiguous heads={len(rep.ambiguous_heads)} rows={rep.ambiguous_rows} "
+          f"of {rep.rows_checked}", flush=True)
 
 
 @pytest.mark.parametrize("layer", [0, 7, 15, 23, 31])
@@ -655,9 +663,11 @@ def test_256k_layer_sampled_rows(layer):
     seed l): every head's last-block mass and budget, and the scores, lists
     and attention of 512 sampled query rows per head (the same rows for every
     head) and of their block rows."""
+    from tests import pregen
     wl = WORKLOADS["llama3_8b_n262144"].replace(seed=layer)
     print(f"\n[256K layer {layer}]", flush=True)
-    _sampled_rows_check(wl, 512)
+    pg = pregen.active()
+    _sampled_rows_check(wl, 512, pg.get(layer) if pg is not None else None)
 
 
 def test_maximum_size_sampled_rows():
