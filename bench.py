@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--noise", type=float, default=None, help="head deviation sigma")
     ap.add_argument("--num-proxy-groups", type=int, default=None)
     ap.add_argument("--min-budget", type=int, default=None)
+    ap.add_argument("--seq-len", type=int, default=None,
+                    help="override the workload's sequence length (same recipe and seed)")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -843,6 +845,9 @@ def main():
         kw["num_proxy_groups"] = args.num_proxy_groups
     if args.min_budget is not None:
         kw["min_budget_tokens"] = args.min_budget
+    if args.seq_len is not None:
+        kw["seq_len"] = args.seq_len
+        kw["name"] = f"{wl.name.rsplit('_n', 1)[0]}_n{args.seq_len}"
     wl = wl.replace(**kw) if kw else wl
     r, g, dev_inputs = measure(wl, args.steps, args.warmup, args.dense_steps,
                                with_dense=not args.no_dense)

@@ -246,13 +246,9 @@ int proxyattn_estimate(const proxyattn_problem* p, const void* q, const void* k,
     PA_TRY(check_ws(sh, workspace, workspace_bytes, &L));
     hipStream_t st = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    PA_LAUNCH(launch_pool(sh, q, k, ws + L.qg, ws + L.kg, st), "pool");
-    PA_LAUNCH(launch_est_rowmax(sh, ws + L.qg, ws + L.kg, (float*)(ws + L.rbm),
-                                (float2*)(ws + L.rowpart), st), "est_rowmax");
-    PA_LAUNCH(launch_est_reduce(sh, (const float*)(ws + L.rbm), (const float2*)(ws + L.rowpart),
-                                block_logscore, st), "est_reduce");
-    PA_LAUNCH(launch_mass(sh, q, k, (float2*)(ws + L.part), (float*)(ws + L.lnorm), lastblk_mass, st),
-              "mass");
+    const EstWs w{ws + L.qg, ws + L.kg, (float*)(ws + L.rbm), (float2*)(ws + L.rowpart),
+                  (float2*)(ws + L.part), (float*)(ws + L.lnorm)};
+    PA_LAUNCH(launch_estimate(sh, q, k, w, block_logscore, lastblk_mass, st), "estimate");
     return PROXYATTN_OK;
 }
 

@@ -1,5 +1,14 @@
-// Block scoring (Sec. 3.1, Eq. 1) and the last-block attention mass the
+// Block scoring (Sec. 3.1, Eq. 1-2) and the last-block attention mass the
 // per-head budget is read from (Alg. 1, first two steps).
+//
+// Proxy-head pooling (Sec. 3.1, Eq. 2 and the strided qk-pair dropping that
+// follows it):
+//   Q^g[t'] = fl32(sum_{i in group g, ascending} Q[s t'][i]) * fl32(1/|G|)
+//   K^g[t'] = fl32(sum_{i in group g, ascending} K[s t'][kv(i)]) * fl32(1/|G|)
+// rounded to nearest-even in the problem dtype.  The group's KV keys are
+// summed once per query head of the group, so for GQA the pooled key is the
+// mean of the KV heads of the group's query heads.  Memory-bound: each thread
+// owns one 16-byte slice of one pooled row.
 //
 // All score tiles are computed transposed, S^T = K Q^T, on the 32x32 MFMA
 // tile: lane l then owns one query (column l % 32) and 16 keys of it, so row
@@ -29,6 +38,18 @@
 //   mass_block:  per (head, row, key block) the block's (max, sum of exp2).
 //   mass_norm:   each row's normaliser from its blocks.
 //   mass_sum:    per key block, the sum over rows of the block's share.
+//
+// Launches.  The two chains (pool -> est_rowmax -> est_reduce and
+// mass_block -> mass_norm -> mass_sum) do not depend on each other, so each
+// launch runs one stage of both, the workgroups of the two roles side by side
+// in one grid (horizontal fusion: three launches instead of six, which on
+// short sequences is most of the estimation time; the arithmetic of every
+// output is that of the stage alone):
+//   est_stage1:  pool      + mass_block
+//   est_stage2:  est_rowmax + mass_norm
+//   est_stage3:  est_reduce + mass_sum
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -85,25 +106,75 @@ __device__ __forceinline__ f32x16 st_tile(const T* lds_tile, const typename Frag
 }
 
 // ---------------------------------------------------------------------------
+// a1: pooling.  One 256-thread workgroup per 256 (pooled row, 16-byte slice)
+// pairs; `blk` is the workgroup's index among the pooling workgroups.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__device__ __forceinline__ void pool_body(const Shape& sh, const T* __restrict__ q,
+                                          const T* __restrict__ k, T* __restrict__ qg,
+                                          T* __restrict__ kg, int64_t blk) {
+    constexpr int V = Vec16<T>::n;
+    constexpr int SLICES = D / V;
+    const int64_t gid = blk * 256 + threadIdx.x;
+    const int64_t rows = (int64_t)sh.g * sh.np;
+    if (gid >= rows * SLICES) return;
+    const int slice = (int)(gid % SLICES);
+    const int64_t row = gid / SLICES;
+    const int g = (int)(row / sh.np);
+    const int tp = (int)(row % sh.np);
+    const int64_t t = (int64_t)tp * sh.s;
+    float aq[V], ak[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) { aq[e] = 0.f; ak[e] = 0.f; }
+    for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
+        const T* qp = q + t * sh.q_tok + (int64_t)i * sh.q_head + slice * V;
+        const T* kp = k + t * sh.kv_tok + (int64_t)(i / sh.rep) * sh.kv_head + slice * V;
+        const uint4 qv = *reinterpret_cast<const uint4*>(qp);
+        const uint4 kv = *reinterpret_cast<const uint4*>(kp);
+        const T* qe = reinterpret_cast<const T*>(&qv);
+        const T* ke = reinterpret_cast<const T*>(&kv);
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            aq[e] = aq[e] + to_f32<T>(qe[e]);
+            ak[e] = ak[e] + to_f32<T>(ke[e]);
+        }
+    }
+    uint4 oq, ok;
+    T* oqe = reinterpret_cast<T*>(&oq);
+    T* oke = reinterpret_cast<T*>(&ok);
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+        // separate multiply after the sum: no contraction into an fma
+        const float mq = __fmul_rn(aq[e], sh.inv_gsize);
+        const float mk = __fmul_rn(ak[e], sh.inv_gsize);
+        oqe[e] = from_f32_rne<T>(mq);
+        oke[e] = from_f32_rne<T>(mk);
+    }
+    const int64_t o = ((int64_t)g * sh.np + tp) * D + slice * V;
+    *reinterpret_cast<uint4*>(qg + o) = oq;
+    *reinterpret_cast<uint4*>(kg + o) = ok;
+}
+
+// ---------------------------------------------------------------------------
 // a2: per-(row, key block) max and per-(row, key chunk) (max, sum)
-// grid (ceil(N'/128), est_nc, G), 256 threads; workgroup (x, c) takes the
-// strided rows R0 = (gridDim.x - 1 - x) * 128 .. +127 (longest rows first),
-// wave w rows R0+32w..+31, against key tiles [c est_kc, (c+1) est_kc) of the
-// causal range (chunks past it exit at once).  Only the wave's diagonal key
-// tile needs the causal mask.
+// (ceil(N'/128), est_nc, G) workgroups of 256 threads; workgroup (x, c, g)
+// takes the strided rows R0 = (nbx - 1 - x) * 128 .. +127 (longest rows
+// first), wave w rows R0+32w..+31, against key tiles [c est_kc, (c+1) est_kc)
+// of the causal range (chunks past it exit at once).  Only the wave's
+// diagonal key tile needs the causal mask.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int BP>
-__global__ __launch_bounds__(256, 2) void est_rowmax_kernel(Shape sh, const T* __restrict__ qg,
-                                                            const T* __restrict__ kg,
-                                                            float* __restrict__ rbm,
-                                                            float2* __restrict__ rowpart) {
+__device__ __forceinline__ void est_rowmax_body(const Shape& sh, const T* __restrict__ qg,
+                                                const T* __restrict__ kg,
+                                                float* __restrict__ rbm,
+                                                float2* __restrict__ rowpart, int bx, int c, int g,
+                                                int nbx) {
     typedef typename FragOf<T>::type Frag;
     constexpr int KS = D / 16;
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, 256>::LDT];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
-    const int c = blockIdx.y, g = blockIdx.z;
     const int np = sh.np;
-    const int R0 = (gridDim.x - 1 - blockIdx.x) * 128;
+    const int R0 = (nbx - 1 - bx) * 128;
     const int kt_begin = c * sh.est_kc;
     const T* qbase = qg + (int64_t)g * np * D;
     const T* kbase = kg + (int64_t)g * np * D;
@@ -191,14 +262,14 @@ __global__ __launch_bounds__(256, 2) void est_rowmax_kernel(Shape sh, const T* _
 
 // ---------------------------------------------------------------------------
 // a3: row normalisers and the block max-pool in the log domain.
-// grid (Mq, G), 256 threads.
+// One 256-thread workgroup per (block row m, group g).
 // ---------------------------------------------------------------------------
 template <int BP>
-__global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* __restrict__ rbm,
-                                                         const float2* __restrict__ rowpart,
-                                                         float* __restrict__ logA) {
+__device__ __forceinline__ void est_reduce_body(const Shape& sh, const float* __restrict__ rbm,
+                                                const float2* __restrict__ rowpart,
+                                                float* __restrict__ logA, int m, int g) {
     __shared__ float L[BP];
-    const int m = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+    const int tid = threadIdx.x;
     const int r0 = m * BP;
     const int nr = min(BP, sh.np - r0);
     // the block's rows lie in one 128-row band of est_rowmax (BP divides
@@ -246,22 +317,24 @@ __global__ __launch_bounds__(256) void est_reduce_kernel(Shape sh, const float* 
 
 // ---------------------------------------------------------------------------
 // a4: last-block mass, one pass over the keys.
-// mass_block: grid (nchunks, Hq), B*2 threads (B/32 waves, 32 last-block rows
-//   each).  For every (row, key block) of its key chunk: the block's largest
-//   scaled logit m and the sum of exp2(logit - m) over the block's visible
-//   keys, written to part[i][row][block] (float2).
+// mass_block: one 256-thread workgroup per (key chunk c, head i); wave w
+//   takes last-block rows 32w..32w+31 (b = 64: waves 2 and 3 only help to
+//   stage the key tiles).  For every (row, key block) of its key chunk: the
+//   block's largest scaled logit m and the sum of exp2(logit - m) over the
+//   block's visible keys, written to part[i][row][block] (float2).
 // mass_norm, mass_sum: each row's log2-sum-exp over its visible blocks, then
 //   mass[i][n] = sum over rows of s * exp2(m - L) in a fixed order.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int B>
-__global__ __launch_bounds__(B * 2, 2) void mass_block_kernel(Shape sh, const T* __restrict__ q,
-                                                          const T* __restrict__ k,
-                                                          float2* __restrict__ part) {
+__device__ __forceinline__ void mass_block_body(const Shape& sh, const T* __restrict__ q,
+                                                const T* __restrict__ k,
+                                                float2* __restrict__ part, int c, int i) {
     typedef typename FragOf<T>::type Frag;
-    constexpr int NTH = B * 2;
+    constexpr int NTH = 256;
+    static_assert(B <= 128, "at most 4 waves of 32 last-block rows");
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, NTH>::LDT];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
-    const int c = blockIdx.x, i = blockIdx.y, kvh = i / sh.rep;
+    const int kvh = i / sh.rep;
     const int n = sh.n;
     const int nrows = min(B, n), t0 = n - nrows;
     const int rl = 32 * w + lc, t = t0 + rl;
@@ -326,19 +399,16 @@ __global__ __launch_bounds__(B * 2, 2) void mass_block_kernel(Shape sh, const T*
     }
 }
 
-constexpr int kMassReduceThreads = 1024;   // 16 waves
-
-// Row normalisers: grid (Hq, ceil(rows / 16)), one wave per last-block row:
-// the row's log2-sum-exp over its visible blocks n <= t / b (block n holds
-// key n b <= t, so every one of them was written).
-__global__ __launch_bounds__(kMassReduceThreads) void mass_norm_kernel(Shape sh,
-                                                                      const float2* __restrict__ part,
-                                                                      float* __restrict__ lnorm) {
-    constexpr int NW = kMassReduceThreads / 64;
-    const int i = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+// Row normalisers: one wave per last-block row, 4 rows per 256-thread
+// workgroup (`rg`: the workgroup's index among the head's): the row's
+// log2-sum-exp over its visible blocks n <= t / b (block n holds key n b <= t,
+// so every one of them was written).
+__device__ __forceinline__ void mass_norm_body(const Shape& sh, const float2* __restrict__ part,
+                                               float* __restrict__ lnorm, int i, int rg) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int b = sh.b, mq = sh.mq;
     const int nrows = min(b, sh.n), t0 = sh.n - nrows;
-    const int r = blockIdx.y * NW + w;
+    const int r = rg * 4 + w;
     if (r >= nrows) return;   // whole waves; no barrier follows
     const int nmax = (t0 + r) / b;
     const float2* pr = part + ((int64_t)i * b + r) * mq;
@@ -356,110 +426,175 @@ __global__ __launch_bounds__(kMassReduceThreads) void mass_norm_kernel(Shape sh,
     if (lane == 0) lnorm[(int64_t)i * b + r] = M + log2f(sv);
 }
 
-// Block masses: grid (Hq, ceil(Nk / 64)), 64 blocks per workgroup, one per
-// lane; wave w sums rows w, w + 16, ... and wave 0 adds the 16 partial sums in
-// order (a fixed-order sum).
-__global__ __launch_bounds__(kMassReduceThreads) void mass_sum_kernel(Shape sh,
-                                                                     const float2* __restrict__ part,
-                                                                     const float* __restrict__ lnorm,
-                                                                     float* __restrict__ mass) {
-    constexpr int NW = kMassReduceThreads / 64;
+// Block masses: 64 blocks per 256-thread workgroup (`chunk`), one per lane.
+// The fixed-order sum: partial p (p = 0..15) adds rows p, p + 16, ... in
+// increasing order (wave w computes partials w, w + 4, w + 8, w + 12), then
+// the 16 partials are added in order.
+constexpr int kMassPartials = 16;
+
+__device__ __forceinline__ void mass_sum_body(const Shape& sh, const float2* __restrict__ part,
+                                              const float* __restrict__ lnorm,
+                                              float* __restrict__ mass, int i, int chunk) {
     __shared__ float L[128];
-    __shared__ float ps[NW][64];
-    const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    __shared__ float ps[kMassPartials][64];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int b = sh.b, mq = sh.mq;
     const int nrows = min(b, sh.n), t0 = sh.n - nrows;
-    for (int r = tid; r < nrows; r += kMassReduceThreads) L[r] = lnorm[(int64_t)i * b + r];
+    for (int r = tid; r < nrows; r += 256) L[r] = lnorm[(int64_t)i * b + r];
     __syncthreads();
     const float2* base = part + (int64_t)i * b * mq;
-    const int nb = blockIdx.y * 64 + lane;
-    float acc = 0.f;
-    if (nb < mq) {
-        for (int r = w; r < nrows; r += NW) {
-            if (nb * b <= t0 + r) {
-                const float2 x = base[(int64_t)r * mq + nb];
-                if (x.x != kNegInf) acc += x.y * fast_exp2(x.x - L[r]);
+    const int nb = chunk * 64 + lane;
+#pragma unroll
+    for (int pp = 0; pp < kMassPartials / 4; ++pp) {
+        const int p = w + 4 * pp;
+        float acc = 0.f;
+        if (nb < mq) {
+            for (int r = p; r < nrows; r += kMassPartials) {
+                if (nb * b <= t0 + r) {
+                    const float2 x = base[(int64_t)r * mq + nb];
+                    if (x.x != kNegInf) acc += x.y * fast_exp2(x.x - L[r]);
+                }
             }
         }
+        ps[p][lane] = acc;
     }
-    ps[w][lane] = acc;
     __syncthreads();
     if (w == 0 && nb < mq) {
         float sum = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) sum += ps[ww][lane];
+        for (int p = 0; p < kMassPartials; ++p) sum += ps[p][lane];
         mass[(int64_t)i * mq + nb] = sum;
     }
 }
 
 // ---------------------------------------------------------------------------
-// launchers
+// The three fused launches (1-D grids of 256-thread workgroups; the
+// workgroups of the longer role come first).
 // ---------------------------------------------------------------------------
-template <typename T, int D>
-static hipError_t rowmax_t(const Shape& sh, const void* qg, const void* kg, float* rbm,
-                           float2* rowpart, hipStream_t st) {
-    dim3 grid((sh.np + 127) / 128, sh.est_nc, sh.g);
-    switch (sh.bp) {
-        case 16: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 16>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
-        case 32: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 32>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
-        case 64: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 64>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
-        case 128: hipLaunchKernelGGL((est_rowmax_kernel<T, D, 128>), grid, dim3(256), 0, st, sh, (const T*)qg, (const T*)kg, rbm, rowpart); break;
-        default: return hipErrorInvalidValue;
+struct EstGrid {
+    int pool;      // pooling workgroups
+    int mblock;    // mass_block workgroups: nchunks x Hq
+    int rowmax;    // est_rowmax workgroups: nbx x est_nc x G
+    int nbx;       // 128-row bands of est_rowmax
+    int norm;      // mass_norm workgroups: Hq x ceil(rows / 4)
+    int norm_per;  // per head
+    int reduce;    // est_reduce workgroups: Mq x G
+    int msum;      // mass_sum workgroups: Hq x ceil(Nk / 64)
+    int msum_per;  // per head
+};
+
+template <typename T, int D, int B>
+__global__ __launch_bounds__(256, 2) void est_stage1_kernel(Shape sh, EstGrid eg,
+                                                            const T* __restrict__ q,
+                                                            const T* __restrict__ k,
+                                                            T* __restrict__ qg, T* __restrict__ kg,
+                                                            float2* __restrict__ part) {
+    const int j = blockIdx.x;
+    if (j < eg.mblock) {
+        mass_block_body<T, D, B>(sh, q, k, part, j % sh.nchunks, j / sh.nchunks);
+        return;
     }
-    return hipGetLastError();
+    pool_body<T, D>(sh, q, k, qg, kg, j - eg.mblock);
 }
 
-hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
-                             float2* rowpart, hipStream_t st) {
-    if (sh.dtype == 0)
-        return sh.d == 64 ? rowmax_t<bf16, 64>(sh, qg, kg, rbm, rowpart, st)
-                          : rowmax_t<bf16, 128>(sh, qg, kg, rbm, rowpart, st);
-    return sh.d == 64 ? rowmax_t<float, 64>(sh, qg, kg, rbm, rowpart, st)
-                      : rowmax_t<float, 128>(sh, qg, kg, rbm, rowpart, st);
+template <typename T, int D, int BP>
+__global__ __launch_bounds__(256, 2) void est_stage2_kernel(Shape sh, EstGrid eg,
+                                                            const T* __restrict__ qg,
+                                                            const T* __restrict__ kg,
+                                                            float* __restrict__ rbm,
+                                                            float2* __restrict__ rowpart,
+                                                            const float2* __restrict__ part,
+                                                            float* __restrict__ lnorm) {
+    const int j = blockIdx.x;
+    if (j < eg.rowmax) {
+        const int bx = j % eg.nbx, c = (j / eg.nbx) % sh.est_nc, g = j / (eg.nbx * sh.est_nc);
+        est_rowmax_body<T, D, BP>(sh, qg, kg, rbm, rowpart, bx, c, g, eg.nbx);
+        return;
+    }
+    const int jn = j - eg.rowmax;
+    mass_norm_body(sh, part, lnorm, jn / eg.norm_per, jn % eg.norm_per);
 }
 
-hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* rowpart,
-                             float* logA, hipStream_t st) {
-    dim3 grid(sh.mq, sh.g);
-    switch (sh.bp) {
-        case 16: hipLaunchKernelGGL((est_reduce_kernel<16>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
-        case 32: hipLaunchKernelGGL((est_reduce_kernel<32>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
-        case 64: hipLaunchKernelGGL((est_reduce_kernel<64>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
-        case 128: hipLaunchKernelGGL((est_reduce_kernel<128>), grid, dim3(256), 0, st, sh, rbm, rowpart, logA); break;
-        default: return hipErrorInvalidValue;
+template <int BP>
+__global__ __launch_bounds__(256) void est_stage3_kernel(Shape sh, EstGrid eg,
+                                                         const float* __restrict__ rbm,
+                                                         const float2* __restrict__ rowpart,
+                                                         float* __restrict__ logA,
+                                                         const float2* __restrict__ part,
+                                                         const float* __restrict__ lnorm,
+                                                         float* __restrict__ mass) {
+    const int j = blockIdx.x;
+    if (j < eg.reduce) {
+        est_reduce_body<BP>(sh, rbm, rowpart, logA, j % sh.mq, j / sh.mq);
+        return;
     }
+    const int jm = j - eg.reduce;
+    mass_sum_body(sh, part, lnorm, mass, jm / eg.msum_per, jm % eg.msum_per);
+}
+
+// ---------------------------------------------------------------------------
+// launcher
+// ---------------------------------------------------------------------------
+static EstGrid est_grid(const Shape& sh) {
+    EstGrid e{};
+    constexpr int kVec = 16;   // bytes per pooled slice
+    const int esz = sh.dtype == 0 ? 2 : 4;
+    const int64_t slices = (int64_t)sh.g * sh.np * (sh.d * esz / kVec);
+    e.pool = (int)((slices + 255) / 256);
+    e.mblock = sh.nchunks * sh.hq;
+    e.nbx = (sh.np + 127) / 128;
+    e.rowmax = e.nbx * sh.est_nc * sh.g;
+    e.norm_per = (std::min(sh.b, sh.n) + 3) / 4;
+    e.norm = sh.hq * e.norm_per;
+    e.reduce = sh.mq * sh.g;
+    e.msum_per = (sh.mq + 63) / 64;
+    e.msum = sh.hq * e.msum_per;
+    return e;
+}
+
+template <typename T, int D, int B, int BP>
+static hipError_t est_t(const Shape& sh, const void* q, const void* k, const EstWs& w,
+                        float* logA, float* mass, hipStream_t st) {
+    const EstGrid eg = est_grid(sh);
+    hipLaunchKernelGGL((est_stage1_kernel<T, D, B>), dim3(eg.mblock + eg.pool), dim3(256), 0, st, sh,
+                       eg, (const T*)q, (const T*)k, (T*)w.qg, (T*)w.kg, w.part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((est_stage2_kernel<T, D, BP>), dim3(eg.rowmax + eg.norm), dim3(256), 0, st,
+                       sh, eg, (const T*)w.qg, (const T*)w.kg, w.rbm, w.rowpart,
+                       (const float2*)w.part, w.lnorm);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((est_stage3_kernel<BP>), dim3(eg.reduce + eg.msum), dim3(256), 0, st, sh, eg,
+                       (const float*)w.rbm, (const float2*)w.rowpart, logA,
+                       (const float2*)w.part, (const float*)w.lnorm, mass);
     return hipGetLastError();
 }
 
 template <typename T, int D, int B>
-static hipError_t mass_t(const Shape& sh, const void* q, const void* k, float2* part, float* lnorm,
-                         float* mass, hipStream_t st) {
-    hipLaunchKernelGGL((mass_block_kernel<T, D, B>), dim3(sh.nchunks, sh.hq), dim3(B * 2), 0, st, sh,
-                       (const T*)q, (const T*)k, part);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    constexpr int NW = kMassReduceThreads / 64;
-    hipLaunchKernelGGL(mass_norm_kernel, dim3(sh.hq, (min(sh.b, sh.n) + NW - 1) / NW),
-                       dim3(kMassReduceThreads), 0, st, sh, (const float2*)part, lnorm);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(mass_sum_kernel, dim3(sh.hq, (sh.mq + 63) / 64), dim3(kMassReduceThreads), 0,
-                       st, sh, (const float2*)part, (const float*)lnorm, mass);
-    return hipGetLastError();
+static hipError_t est_bp(const Shape& sh, const void* q, const void* k, const EstWs& w,
+                         float* logA, float* mass, hipStream_t st) {
+    switch (sh.bp) {
+        case 16: return est_t<T, D, B, 16>(sh, q, k, w, logA, mass, st);
+        case 32: return est_t<T, D, B, 32>(sh, q, k, w, logA, mass, st);
+        case 64: return est_t<T, D, B, 64>(sh, q, k, w, logA, mass, st);
+        case 128: return est_t<T, D, B, 128>(sh, q, k, w, logA, mass, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
-hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* lnorm,
-                       float* mass, hipStream_t st) {
+hipError_t launch_estimate(const Shape& sh, const void* q, const void* k, const EstWs& w,
+                           float* logA, float* mass, hipStream_t st) {
     if (sh.dtype == 0) {
-        if (sh.d == 64) return sh.b == 64 ? mass_t<bf16, 64, 64>(sh, q, k, part, lnorm, mass, st)
-                                          : mass_t<bf16, 64, 128>(sh, q, k, part, lnorm, mass, st);
-        return sh.b == 64 ? mass_t<bf16, 128, 64>(sh, q, k, part, lnorm, mass, st)
-                          : mass_t<bf16, 128, 128>(sh, q, k, part, lnorm, mass, st);
+        if (sh.d == 64) return sh.b == 64 ? est_bp<bf16, 64, 64>(sh, q, k, w, logA, mass, st)
+                                          : est_bp<bf16, 64, 128>(sh, q, k, w, logA, mass, st);
+        return sh.b == 64 ? est_bp<bf16, 128, 64>(sh, q, k, w, logA, mass, st)
+                          : est_bp<bf16, 128, 128>(sh, q, k, w, logA, mass, st);
     }
-    if (sh.d == 64) return sh.b == 64 ? mass_t<float, 64, 64>(sh, q, k, part, lnorm, mass, st)
-                                      : mass_t<float, 64, 128>(sh, q, k, part, lnorm, mass, st);
-    return sh.b == 64 ? mass_t<float, 128, 64>(sh, q, k, part, lnorm, mass, st)
-                      : mass_t<float, 128, 128>(sh, q, k, part, lnorm, mass, st);
+    if (sh.d == 64) return sh.b == 64 ? est_bp<float, 64, 64>(sh, q, k, w, logA, mass, st)
+                                      : est_bp<float, 64, 128>(sh, q, k, w, logA, mass, st);
+    return sh.b == 64 ? est_bp<float, 128, 64>(sh, q, k, w, logA, mass, st)
+                      : est_bp<float, 128, 128>(sh, q, k, w, logA, mass, st);
 }
 
 }  // namespace pa

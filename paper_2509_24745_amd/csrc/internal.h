@@ -86,14 +86,19 @@ WsLayout ws_layout(const Shape& sh);
 // Bytes of the blocked K/V copy: [Hkv][Mq][2 b d] elements.
 size_t kv_blocked_bytes(const Shape& sh);
 
-hipError_t launch_pool(const Shape& sh, const void* q, const void* k, void* qg, void* kg,
-                       hipStream_t st);
-hipError_t launch_est_rowmax(const Shape& sh, const void* qg, const void* kg, float* rbm,
-                             float2* rowpart, hipStream_t st);
-hipError_t launch_est_reduce(const Shape& sh, const float* rbm, const float2* rowpart,
-                             float* logA, hipStream_t st);
-hipError_t launch_mass(const Shape& sh, const void* q, const void* k, float2* part, float* lnorm,
-                       float* mass, hipStream_t st);
+// Workspace regions the estimation launches use.
+struct EstWs {
+    void* qg;          // pooled proxy queries
+    void* kg;          // pooled proxy keys
+    float* rbm;        // per-(row, key block) maxima
+    float2* rowpart;   // per-(row, key chunk) (max, sum)
+    float2* part;      // last-block (max, sum) per (head, row, key block)
+    float* lnorm;      // last-block rows' log2-sum-exp
+};
+// Pooling, proxy block scores (logA [G][Mq][Nk]) and last-block masses
+// (mass [Hq][Nk]) in three launches.
+hipError_t launch_estimate(const Shape& sh, const void* q, const void* k, const EstWs& w,
+                           float* logA, float* mass, hipStream_t st);
 hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int min_blocks,
                          int* head_count, hipStream_t st);
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
