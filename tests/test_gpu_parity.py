@@ -609,13 +609,15 @@ def test_whole_step_replays_from_a_hip_graph():
             assert torch.equal(getattr(bufs, n), ref[n]), f"replay {rep}: {n} differs"
 
 
-def _sampled_rows_check(wl, nsample: int, pre: dict | None = None):
+def _sampled_rows_check(wl, nsample: int, pre: dict | None = None, pool=None):
     """The whole path at full size, in the benchmark's launch configuration:
     pooled heads bit-exact, every head's last-block mass and budget, and the
     proxy scores, lists and attention of seeded sampled query rows (always
     including the last row) and their block rows.  `pre`: the layer's inputs
     and the oracle's pooled heads, block scores of those block rows and
-    masses, prepared ahead (tests/pregen.py); computed here when absent."""
+    masses, prepared ahead (tests/pregen.py); computed here when absent.
+    `pool`: the preparing processes, which then also run the oracle's
+    attention of the sampled rows, split over groups of KV heads."""
     U = _gpu()
     from tests import pregen
     rows = pregen.sample_rows(wl.seq_len, nsample)
@@ -646,10 +648,18 @@ def _sampled_rows_check(wl, nsample: int, pre: dict | None = None):
     C.check_counts(gpu["counts"], counts, cums, wl.gamma, wl.min_budget_tokens, wl.block_size, rep)
     C.check_lists(gpu["block_count"], gpu["block_index"], oa, gpu["counts"], wl.num_q_heads,
                   rows=brows, report=rep)
-    ref_out, ref_lse = O.block_sparse_attention(q, k, v, gpu["block_count"], gpu["block_index"],
-                                                wl.block_size, sc, query_rows=rows)
-    C.check_attention(gpu["out"], ref_out[rows], rep)
-    dl = float(np.abs(gpu["lse"] - ref_lse[:, rows]).max())
+    if pool is None:
+        ref_out, ref_lse = O.block_sparse_attention(q, k, v, gpu["block_count"],
+                                                    gpu["block_index"], wl.block_size, sc,
+                                                    query_rows=rows)
+        ref_out, ref_lse = ref_out[rows], ref_lse[:, rows]
+    else:
+        ref_out, ref_lse = pool.attention(wl.seed, wl.block_size, wl.num_q_heads,
+                                          wl.num_kv_heads, rows, gpu["block_count"],
+                                          gpu["block_index"])
+        pool.release(wl.seed)
+    C.check_attention(gpu["out"], ref_out, rep)
+    dl = float(np.abs(gpu["lse"] - ref_lse).max())
     assert dl <= LSE_TOL, f"max |dlse| = {dl}"
     print(f"\n[{wl.name} seed {wl.seed}] |dlogA|={dla:.2e} |dmass|/rows={dm:.2e} "
           f"max|dO|={rep.max_abs:.2e} mean|dO|={rep.mean_abs:.2e} |dlse|={dl:.2e} "
@@ -667,7 +677,7 @@ def test_256k_layer_sampled_rows(layer):
     wl = WORKLOADS["llama3_8b_n262144"].replace(seed=layer)
     print(f"\n[256K layer {layer}]", flush=True)
     pg = pregen.active()
-    _sampled_rows_check(wl, 512, pg.get(layer) if pg is not None else None)
+    _sampled_rows_check(wl, 512, pg.get(layer) if pg is not None else None, pg)
 
 
 def test_maximum_size_sampled_rows():
