@@ -108,14 +108,18 @@ typedef struct proxyattn_problem {
  * C = key chunks of the block scoring, at most ceil(N'/4096)):
  *   pooled Q^g and K^g      2 * G * N' * d * esz
  *   row (max, sum) pairs    G * C * N' * 8
- *   per-(row, block) maxima G * Mq(Mq+1)/2 * b' * 4
+ *   per-(row, block) maxima G * P * b' * 4
  *   last-block pairs        Hq * b * Mq * 8, plus Hq * b * 4
  *   blocked K/V copy        Hkv * Mq * 2 * b * d * esz
  *   work-queue counters     1024
- * The per-(row, block) maxima grow with the square of the sequence length:
- * 268 MB at N = 131072 with G = 4, b' = 32; 4.3 GB per proxy group at the
- * largest accepted size (Mq = 8192, b' = 32), 17 GB per group with s = 1 and
- * b = 128.  A caller that cannot provide that much must shorten the problem.
+ * P is the number of lower-triangular block pairs (m, n <= m) of one group
+ * of block rows.  The estimation produces and reduces the per-(row, block)
+ * maxima one group at a time; a group is a run of consecutive bands of 128
+ * strided rows, grown while G * P * b' * 4 stays within 512 MiB (a single
+ * band always forms one).  Up to N = 131072 with G = 4 and b' = 32 one group
+ * covers every row (P = Mq(Mq+1)/2, 268 MB); longer problems take several
+ * groups, and the region stays near 512 MiB instead of growing with the
+ * square of the sequence length.
  */
 int proxyattn_workspace_size(const proxyattn_problem* p, size_t* bytes);
 

@@ -154,6 +154,36 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     return PROXYATTN_OK;
 }
 
+// Band groups: consecutive 128-row bands (128 / b' block rows each) whose
+// block rows' lower-triangular pairs, over all proxy groups, fit
+// kRbmMaxBytes (a single band always forms a group).  Greedy from the first
+// band.
+static int rbm_walk(const Shape& sh, int want, RbmGroup* out, int64_t* max_pairs) {
+    const int nbands = (sh.np + 127) / 128;
+    const int rpb = 128 / sh.bp;
+    const int64_t cap = (int64_t)(kRbmMaxBytes / ((size_t)sh.g * sh.bp * 4));
+    auto pairs = [&](int xb0, int xb1) {
+        const int64_t m0 = (int64_t)xb0 * rpb, m1 = std::min((int64_t)xb1 * rpb, (int64_t)sh.mq);
+        return m1 * (m1 + 1) / 2 - m0 * (m0 + 1) / 2;
+    };
+    int k = 0, xb0 = 0;
+    int64_t mx = 0;
+    while (xb0 < nbands) {
+        int xb1 = xb0 + 1;
+        while (xb1 < nbands && pairs(xb0, xb1 + 1) <= cap) ++xb1;
+        mx = std::max(mx, pairs(xb0, xb1));
+        if (k == want && out) { out->xb0 = xb0; out->xb1 = xb1; }
+        ++k;
+        xb0 = xb1;
+    }
+    if (max_pairs) *max_pairs = mx;
+    return k;
+}
+
+int rbm_groups(const Shape& sh, int64_t* max_pairs) { return rbm_walk(sh, -1, nullptr, max_pairs); }
+
+void rbm_group(const Shape& sh, int k, RbmGroup* out) { rbm_walk(sh, k, out, nullptr); }
+
 size_t kv_blocked_bytes(const Shape& sh) {
     const size_t esz = sh.dtype == PROXYATTN_BF16 ? 2 : 4;
     return (size_t)sh.hkv * sh.mq * 2 * sh.d * sh.b * esz;
@@ -166,7 +196,9 @@ WsLayout ws_layout(const Shape& sh) {
     L.qg = off;   off = align_up(off + (size_t)sh.g * sh.np * sh.d * esz);
     L.kg = off;   off = align_up(off + (size_t)sh.g * sh.np * sh.d * esz);
     L.rowpart = off; off = align_up(off + (size_t)sh.g * sh.est_nc * sh.np * 8);
-    L.rbm = off;  off = align_up(off + (size_t)sh.g * ((size_t)sh.mq * (sh.mq + 1) / 2) * sh.bp * 4);
+    int64_t pairs = 0;
+    rbm_groups(sh, &pairs);
+    L.rbm = off;  off = align_up(off + (size_t)sh.g * (size_t)pairs * sh.bp * 4);
     L.part = off; off = align_up(off + (size_t)sh.hq * sh.b * sh.mq * 8);
     L.lnorm = off; off = align_up(off + (size_t)sh.hq * sh.b * 4);
     L.kvb = off;  off = align_up(off + kv_blocked_bytes(sh));

@@ -48,6 +48,9 @@
 //   est_stage1:  pool      + mass_block
 //   est_stage2:  est_rowmax + mass_norm
 //   est_stage3:  est_reduce + mass_sum
+// On long sequences stages 2 and 3 repeat per group of row bands, so that
+// the per-(row, block) maxima they pass on need a bounded region (the mass
+// stages run with the first group).
 #include <algorithm>
 
 #include "common.h"
@@ -157,24 +160,25 @@ __device__ __forceinline__ void pool_body(const Shape& sh, const T* __restrict__
 
 // ---------------------------------------------------------------------------
 // a2: per-(row, key block) max and per-(row, key chunk) (max, sum)
-// (ceil(N'/128), est_nc, G) workgroups of 256 threads; workgroup (x, c, g)
-// takes the strided rows R0 = (nbx - 1 - x) * 128 .. +127 (longest rows
-// first), wave w rows R0+32w..+31, against key tiles [c est_kc, (c+1) est_kc)
-// of the causal range (chunks past it exit at once).  Only the wave's
-// diagonal key tile needs the causal mask.
+// One 256-thread workgroup per (128-row band, key chunk c, group g): it
+// takes the strided rows R0 .. R0+127, wave w rows R0+32w..+31, against key
+// tiles [c est_kc, (c+1) est_kc) of the causal range (chunks past it exit at
+// once).  Only the wave's diagonal key tile needs the causal mask.  The
+// per-(row, key block) maxima go to the current band group's rbm region:
+// lower-triangular pairs (m, n) at tri_index(m, n) - tri_base, tri_count
+// pairs per proxy group.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int BP>
 __device__ __forceinline__ void est_rowmax_body(const Shape& sh, const T* __restrict__ qg,
                                                 const T* __restrict__ kg,
                                                 float* __restrict__ rbm,
-                                                float2* __restrict__ rowpart, int bx, int c, int g,
-                                                int nbx) {
+                                                float2* __restrict__ rowpart, int R0, int c, int g,
+                                                int64_t tri_base, int64_t tri_count) {
     typedef typename FragOf<T>::type Frag;
     constexpr int KS = D / 16;
     __shared__ __attribute__((aligned(16))) T tiles[2][32 * KeyTile<T, D, 256>::LDT];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, lc = lane & 31;
     const int np = sh.np;
-    const int R0 = (nbx - 1 - bx) * 128;
     const int kt_begin = c * sh.est_kc;
     const T* qbase = qg + (int64_t)g * np * D;
     const T* kbase = kg + (int64_t)g * np * D;
@@ -193,8 +197,7 @@ __device__ __forceinline__ void est_rowmax_body(const Shape& sh, const T* __rest
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qf[ks] = load_frag<T>(qrow + 16 * ks + 8 * h);
     }
-    const int64_t tri_total = (int64_t)sh.mq * (sh.mq + 1) / 2;
-    float* rbm_g = rbm + (int64_t)g * tri_total * BP;
+    float* rbm_g = rbm + ((int64_t)g * tri_count - tri_base) * BP;
 
     // running max m (scaled, log2 units) and sum l of exp2(c' s - m)
     float m = kNegInf, l = 0.f, bm = kNegInf;
@@ -267,7 +270,8 @@ __device__ __forceinline__ void est_rowmax_body(const Shape& sh, const T* __rest
 template <int BP>
 __device__ __forceinline__ void est_reduce_body(const Shape& sh, const float* __restrict__ rbm,
                                                 const float2* __restrict__ rowpart,
-                                                float* __restrict__ logA, int m, int g) {
+                                                float* __restrict__ logA, int m, int g,
+                                                int64_t tri_base, int64_t tri_count) {
     __shared__ float L[BP];
     const int tid = threadIdx.x;
     const int r0 = m * BP;
@@ -292,8 +296,7 @@ __device__ __forceinline__ void est_reduce_body(const Shape& sh, const float* __
         L[j] = v;
     }
     __syncthreads();
-    const int64_t tri_total = (int64_t)sh.mq * (sh.mq + 1) / 2;
-    const float* base = rbm + ((int64_t)g * tri_total + tri_index(m, 0)) * BP;
+    const float* base = rbm + ((int64_t)g * tri_count + tri_index(m, 0) - tri_base) * BP;
     float* out = logA + ((int64_t)g * sh.mq + m) * sh.mq;
     for (int n = tid; n < sh.mq; n += 256) {
         float v = kNegInf;
@@ -474,13 +477,17 @@ __device__ __forceinline__ void mass_sum_body(const Shape& sh, const float2* __r
 struct EstGrid {
     int pool;      // pooling workgroups
     int mblock;    // mass_block workgroups: nchunks x Hq
-    int rowmax;    // est_rowmax workgroups: nbx x est_nc x G
-    int nbx;       // 128-row bands of est_rowmax
-    int norm;      // mass_norm workgroups: Hq x ceil(rows / 4)
+    int rowmax;    // est_rowmax workgroups: nbx x est_nc x G (of the band group)
+    int nbx;       // 128-row bands of est_rowmax in the band group
+    int xb1;       // one past the group's last band (bands run longest first)
+    int norm;      // mass_norm workgroups: Hq x ceil(rows / 4) (first group only)
     int norm_per;  // per head
-    int reduce;    // est_reduce workgroups: Mq x G
-    int msum;      // mass_sum workgroups: Hq x ceil(Nk / 64)
+    int reduce;    // est_reduce workgroups: the group's block rows x G
+    int m0, nm;    // the group's block rows [m0, m0 + nm)
+    int msum;      // mass_sum workgroups: Hq x ceil(Nk / 64) (first group only)
     int msum_per;  // per head
+    int64_t tri_base;   // tri_index(m0, 0)
+    int64_t tri_count;  // lower-triangular pairs of the group's block rows
 };
 
 template <typename T, int D, int B>
@@ -508,7 +515,8 @@ __global__ __launch_bounds__(256, 2) void est_stage2_kernel(Shape sh, EstGrid eg
     const int j = blockIdx.x;
     if (j < eg.rowmax) {
         const int bx = j % eg.nbx, c = (j / eg.nbx) % sh.est_nc, g = j / (eg.nbx * sh.est_nc);
-        est_rowmax_body<T, D, BP>(sh, qg, kg, rbm, rowpart, bx, c, g, eg.nbx);
+        est_rowmax_body<T, D, BP>(sh, qg, kg, rbm, rowpart, (eg.xb1 - 1 - bx) * 128, c, g,
+                                  eg.tri_base, eg.tri_count);
         return;
     }
     const int jn = j - eg.rowmax;
@@ -525,7 +533,8 @@ __global__ __launch_bounds__(256) void est_stage3_kernel(Shape sh, EstGrid eg,
                                                          float* __restrict__ mass) {
     const int j = blockIdx.x;
     if (j < eg.reduce) {
-        est_reduce_body<BP>(sh, rbm, rowpart, logA, j % sh.mq, j / sh.mq);
+        est_reduce_body<BP>(sh, rbm, rowpart, logA, eg.m0 + j % eg.nm, j / eg.nm, eg.tri_base,
+                            eg.tri_count);
         return;
     }
     const int jm = j - eg.reduce;
@@ -542,33 +551,58 @@ static EstGrid est_grid(const Shape& sh) {
     const int64_t slices = (int64_t)sh.g * sh.np * (sh.d * esz / kVec);
     e.pool = (int)((slices + 255) / 256);
     e.mblock = sh.nchunks * sh.hq;
-    e.nbx = (sh.np + 127) / 128;
-    e.rowmax = e.nbx * sh.est_nc * sh.g;
     e.norm_per = (std::min(sh.b, sh.n) + 3) / 4;
     e.norm = sh.hq * e.norm_per;
-    e.reduce = sh.mq * sh.g;
     e.msum_per = (sh.mq + 63) / 64;
     e.msum = sh.hq * e.msum_per;
     return e;
 }
 
+// Band group k of est_rowmax / est_reduce (see rbm_groups): bands [xb0, xb1)
+// of 128 strided rows, block rows [m0, m1).
+static void set_group(const Shape& sh, const RbmGroup& gr, bool first, EstGrid* e) {
+    const int rows_per_band = 128 / sh.bp;   // block rows per 128-row band
+    e->xb1 = gr.xb1;
+    e->nbx = gr.xb1 - gr.xb0;
+    e->rowmax = e->nbx * sh.est_nc * sh.g;
+    e->m0 = gr.xb0 * rows_per_band;
+    const int m1 = std::min(gr.xb1 * rows_per_band, sh.mq);
+    e->nm = m1 - e->m0;
+    e->reduce = e->nm * sh.g;
+    e->tri_base = (int64_t)e->m0 * (e->m0 + 1) / 2;
+    e->tri_count = (int64_t)m1 * (m1 + 1) / 2 - e->tri_base;
+    if (!first) e->norm = e->msum = 0;
+}
+
 template <typename T, int D, int B, int BP>
 static hipError_t est_t(const Shape& sh, const void* q, const void* k, const EstWs& w,
                         float* logA, float* mass, hipStream_t st) {
-    const EstGrid eg = est_grid(sh);
+    EstGrid eg = est_grid(sh);
     hipLaunchKernelGGL((est_stage1_kernel<T, D, B>), dim3(eg.mblock + eg.pool), dim3(256), 0, st, sh,
                        eg, (const T*)q, (const T*)k, (T*)w.qg, (T*)w.kg, w.part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((est_stage2_kernel<T, D, BP>), dim3(eg.rowmax + eg.norm), dim3(256), 0, st,
-                       sh, eg, (const T*)w.qg, (const T*)w.kg, w.rbm, w.rowpart,
-                       (const float2*)w.part, w.lnorm);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((est_stage3_kernel<BP>), dim3(eg.reduce + eg.msum), dim3(256), 0, st, sh, eg,
-                       (const float*)w.rbm, (const float2*)w.rowpart, logA,
-                       (const float2*)w.part, (const float*)w.lnorm, mass);
-    return hipGetLastError();
+    // est_rowmax writes and est_reduce reads the per-(row, block) maxima one
+    // band group at a time, so that their region stays bounded (one group,
+    // the whole range, unless it would exceed kRbmMaxBytes); the mass
+    // stages ride along with the first group
+    const int ngroups = rbm_groups(sh, nullptr);
+    for (int k = 0; k < ngroups; ++k) {
+        RbmGroup gr;
+        rbm_group(sh, k, &gr);
+        set_group(sh, gr, k == 0, &eg);
+        hipLaunchKernelGGL((est_stage2_kernel<T, D, BP>), dim3(eg.rowmax + eg.norm), dim3(256), 0,
+                           st, sh, eg, (const T*)w.qg, (const T*)w.kg, w.rbm, w.rowpart,
+                           (const float2*)w.part, w.lnorm);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((est_stage3_kernel<BP>), dim3(eg.reduce + eg.msum), dim3(256), 0, st, sh,
+                           eg, (const float*)w.rbm, (const float2*)w.rowpart, logA,
+                           (const float2*)w.part, (const float*)w.lnorm, mass);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 template <typename T, int D, int B>

@@ -66,12 +66,26 @@ constexpr int kFillGroups = 1024;
 // band's chain of tiles (up to N'/32) would set the kernel's time.
 constexpr int kEstMaxTiles = 128;
 
+// Largest region of per-(row, key block) maxima the estimation keeps at once:
+// longer problems produce and reduce them one group of row bands at a time.
+constexpr size_t kRbmMaxBytes = (size_t)512 << 20;
+
+// A group of est_rowmax's 128-strided-row bands [xb0, xb1).
+struct RbmGroup {
+    int xb0, xb1;
+};
+// Number of band groups (and, if max_pairs is not NULL, the largest group's
+// lower-triangular block pairs per proxy group); rbm_group gives group k.
+int rbm_groups(const Shape& sh, int64_t* max_pairs);
+void rbm_group(const Shape& sh, int k, RbmGroup* out);
+
 // Byte offsets of the workspace regions (each 256-byte aligned).
 struct WsLayout {
     size_t qg, kg;   // pooled proxy heads [G][N'][d] (problem dtype)
     size_t rowpart;  // proxy rows' per-chunk (max, sum of exp2) [G][est_nc][N'] float2
-    size_t rbm;      // per-(row, key block) max of the scaled proxy logits,
-                     // [G][Mq(Mq+1)/2][b'] fp32 (lower-triangular block pairs)
+    size_t rbm;      // per-(row, key block) max of the scaled proxy logits of one band
+                     // group, [G][pairs][b'] fp32 (lower-triangular block pairs
+                     // of the group's block rows)
     size_t part;     // last-block (max, sum) per (head, row, key block) [Hq][b][Mq] float2
     size_t lnorm;    // last-block rows' log2-sum-exp [Hq][b] fp32
     size_t kvb;      // re-blocked K and V^T [Hkv][Mq][2 b d] (problem dtype)

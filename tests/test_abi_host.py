@@ -152,41 +152,88 @@ def test_key_chunk_rule():
     assert _key_chunks(2048, 32, 4, 128, 4) == (128, 16, 4, 4)
 
 
+RBM_MAX_BYTES = 512 << 20
+
+
+def _rbm_pairs(n, g, b, s):
+    """The library's band groups of the per-(row, key block) maxima:
+    consecutive bands of 128 strided rows (128 / b' block rows each), grown
+    greedily while the group's lower-triangular block pairs over all proxy
+    groups fit 512 MiB.  Returns (groups, largest group's pairs)."""
+    npr, mq, bp = -(-n // s), -(-n // b), b // s
+    nb, rpb = -(-npr // 128), 128 // bp
+    cap = RBM_MAX_BYTES // (g * bp * 4)
+
+    def pairs(x0, x1):
+        m0, m1 = x0 * rpb, min(x1 * rpb, mq)
+        return m1 * (m1 + 1) // 2 - m0 * (m0 + 1) // 2
+
+    groups, mx, x0 = 0, 0, 0
+    while x0 < nb:
+        x1 = x0 + 1
+        while x1 < nb and pairs(x0, x1 + 1) <= cap:
+            x1 += 1
+        mx = max(mx, pairs(x0, x1))
+        groups += 1
+        x0 = x1
+    return groups, mx
+
+
+def test_rbm_band_groups():
+    """One group up to 128K with 4 proxy groups (the region is the whole
+    lower triangle, 268 MB); longer problems split into groups whose region
+    stays within 512 MiB."""
+    assert _rbm_pairs(131072, 4, 128, 4) == (1, 1024 * 1025 // 2)
+    g256, p256 = _rbm_pairs(262144, 4, 128, 4)
+    assert g256 >= 2 and 4 * p256 * 32 * 4 <= RBM_MAX_BYTES
+    g1m, p1m = _rbm_pairs(8192 * 128, 4, 128, 4)
+    assert g1m > 8 and 4 * p1m * 32 * 4 <= RBM_MAX_BYTES
+    g1, p1 = _rbm_pairs(8192 * 128, 1, 128, 1)       # b' = 128
+    assert 1 * p1 * 128 * 4 <= RBM_MAX_BYTES
+
+
 @pytest.mark.parametrize("n,hq,hkv,g,b,s", [
-    (32768, 32, 8, 4, 128, 4), (8192, 32, 8, 4, 128, 4), (131072, 32, 8, 4, 128, 4),
+    (32768, 32, 8, 4, 128, 4), (262144, 32, 8, 4, 128, 4), (8192 * 128, 8, 2, 2, 128, 4),
+    (8192 * 128, 8, 2, 1, 128, 1), (8192, 32, 8, 4, 128, 4), (131072, 32, 8, 4, 128, 4),
     (65536, 28, 4, 2, 128, 4), (3000, 8, 2, 2, 64, 2), (777, 4, 4, 1, 64, 1)])
 def test_workspace_size_formula(n, hq, hkv, g, b, s):
     _lib()
-    d = 128
     prob = _prob(seq_len=n, num_q_heads=hq, num_kv_heads=hkv, num_proxy_groups=g,
                  block_size=b, stride=s)
+    assert pa.proxyattn_workspace_size(prob) == _expected_ws(n, hq, hkv, g, b, s)
+
+
+def _expected_ws(n, hq, hkv, g, b, s, d=128):
+    """The workspace regions as the header states them, each rounded up to
+    256 bytes; the head-overlap diagnostic's region reuses the K/V copy's."""
     npr, mq, bp = -(-n // s), -(-n // b), b // s
     _, _, _, est_nc = _key_chunks(n, hq, g, b, s)
     regions = [g * npr * d * 2, g * npr * d * 2, g * est_nc * npr * 8,
-               g * (mq * (mq + 1) // 2) * bp * 4, hq * b * mq * 8, hq * b * 4,
+               g * _rbm_pairs(n, g, b, s)[1] * bp * 4, hq * b * mq * 8, hq * b * 4,
                hkv * mq * 2 * d * b * 2, 8 * 32 * 4]
     end = sum(-(-r // 256) * 256 for r in regions)
     kvb = sum(-(-r // 256) * 256 for r in regions[:6])
     diag_end = kvb + -(-(hq * n * 4) // 256) * 256 + -(-(hq * 8) // 256) * 256
-    assert pa.proxyattn_workspace_size(prob) == max(end, diag_end)
+    return max(end, diag_end)
 
 
 def test_workspace_size_at_the_largest_problem():
-    """8192 blocks: the per-(row, block) maxima dominate (G * Mq(Mq+1)/2 * b'
-    floats), 4.3 GB per proxy group with b' = 32 and 17 GB with s = 1."""
+    """8192 blocks: the per-(row, block) maxima are produced and reduced one
+    group of row bands at a time, so their region stays within 512 MiB
+    (the whole lower triangle would be 4.3 GB per proxy group with b' = 32
+    and 17 GB with s = 1)."""
     _lib()
     mq = 8192
     for g, s, bp in ((1, 4, 32), (4, 4, 32), (1, 1, 128)):
         prob = _prob(seq_len=mq * 128, num_q_heads=32, num_kv_heads=8, num_proxy_groups=g,
                      stride=s)
         ws = pa.proxyattn_workspace_size(prob)
-        rbm = g * (mq * (mq + 1) // 2) * bp * 4
-        assert ws > rbm
-        assert ws < rbm + 4 * 2**30 * g + 3 * 2**30     # the other regions are a few GB
-        if (g, s) == (1, 4):
-            assert 4.2e9 < rbm < 4.4e9
-        if s == 1:
-            assert 17e9 < rbm < 17.3e9
+        whole = g * (mq * (mq + 1) // 2) * bp * 4
+        assert whole > 4e9
+        groups, pairs = _rbm_pairs(mq * 128, g, 128, s)
+        assert groups > 1 and g * pairs * bp * 4 <= RBM_MAX_BYTES
+        assert ws == _expected_ws(mq * 128, 32, 8, g, 128, s)
+        assert ws < _expected_ws(mq * 128, 32, 8, g, 128, s) - g * pairs * bp * 4 + whole
 
 
 def test_workspace_size_of_empty_problem():
