@@ -64,8 +64,9 @@ def parse():
                     help="time a stack of LAYERS layers of --workload (layer l drawn with seed l; "
                          "one JSON line per layer, then the totals)")
     ap.add_argument("--ttft", action="store_true",
-                    help="with --stack: add a decoder layer's non-attention work per layer and "
-                         "report the prefill time-to-first-token, sparse vs dense attention")
+                    help="with --stack: run a LAYERS-layer decoder prefill around the path "
+                         "(projections, RoPE, MLP; one timed region) and report the "
+                         "time-to-first-token with the sparse path vs the dense kernel")
     ap.add_argument("--stack-workers", type=int, default=4,
                     help="processes generating stack layers ahead of the GPU")
     ap.add_argument("--profile-summary", metavar="DIR", default=None,
@@ -471,58 +472,147 @@ def summary_line(wl, r, steps):
     }
 
 
-def decoder_nonattn_ms(n: int, hidden: int = 4096, hq: int = 32, hkv: int = 8, d: int = 128,
-                       inter: int = 14336, reps: int = 3, rope_theta: float = 500000.0) -> float:
-    """Milliseconds of the non-attention work of one Llama-3-8B-shaped decoder
-    layer at n tokens in bf16 with random weights: RMSNorm, QKV projection,
-    RoPE on q and k, output projection, residual, RMSNorm, gate/up
-    projection, SiLU gate, down projection, residual.  Library GEMMs and
-    torch element-wise ops (the layer around the attention; the attention
-    itself is timed separately on structured inputs)."""
-    import torch
-    bf = torch.bfloat16
-    dev = "cuda"
-    g = torch.Generator(device=dev).manual_seed(0)
-    x = torch.randn(n, hidden, device=dev, dtype=bf, generator=g)
-    w_qkv = torch.randn(hidden, (hq + 2 * hkv) * d, device=dev, dtype=bf, generator=g) * hidden ** -0.5
-    w_o = torch.randn(hq * d, hidden, device=dev, dtype=bf, generator=g) * (hq * d) ** -0.5
-    w_gu = torch.randn(hidden, 2 * inter, device=dev, dtype=bf, generator=g) * hidden ** -0.5
-    w_dn = torch.randn(inter, hidden, device=dev, dtype=bf, generator=g) * inter ** -0.5
-    attn_out = torch.randn(n, hq * d, device=dev, dtype=bf, generator=g)
-    nrm1 = torch.ones(hidden, device=dev, dtype=bf)
-    nrm2 = torch.ones(hidden, device=dev, dtype=bf)
-    inv = 1.0 / (rope_theta ** (torch.arange(0, d, 2, device=dev, dtype=torch.float32) / d))
-    ang = torch.arange(n, device=dev, dtype=torch.float32)[:, None] * inv[None, :]
-    cos, sin = ang.cos().to(bf)[:, None, :], ang.sin().to(bf)[:, None, :]
+DECODER_ALPHA = 0.125
 
-    def rms(t, w):
+
+class DecoderPrefill:
+    """A Llama-3-8B-shaped decoder prefill in bf16 whose attention is the
+    ProxyAttn path or, for the baseline, the dense kernel (the paper's
+    end-to-end prefill setting, Sec. 4.3 and Fig. 1, with random weights).
+
+    Layer l, on one stream:
+        h = RMSNorm(x);  [q' | k' | v'] = h W_qkv;  RoPE on q' and k';
+        Q = Qs + alpha q',  K = Ks + alpha k',  V = Vs + alpha v';
+        o = attention(Q, K, V)          (estimate, select, prepare_kv and the
+                                         sparse call, or prepare_kv and the
+                                         dense call);
+        x = x + o W_o;  [g | u] = RMSNorm(x) W_gu;  x = x + (SiLU(g) u) W_down.
+    Qs, Ks, Vs are layer l's structured synthetic inputs.  Random weights on
+    random hidden states give attention with no block structure, so the
+    structure comes from the synthetic recipe and the projections are added
+    to it: every attention reads what its layer's projections wrote, its
+    output feeds the output projection, and each layer's hidden state is the
+    next layer's input.  Weights are drawn per layer (about 0.44 GB a layer
+    at the Llama-3-8B sizes), inputs and weights stay resident in HBM.
+    """
+
+    def __init__(self, wl, structured, hidden: int = 4096, inter: int = 14336,
+                 alpha: float = DECODER_ALPHA, seed: int = 0, rope_theta: float = 500000.0):
+        import torch
+        from paper_2509_24745_amd import proxyattn as pa
+        self.torch, self.pa, self.wl = torch, pa, wl
+        self.hidden, self.inter, self.alpha = hidden, inter, alpha
+        n, hq, hkv, d = wl.seq_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+        self.n, self.hq, self.hkv, self.d = n, hq, hkv, d
+        for qs, ks, vs in structured:
+            if (tuple(qs.shape) != (n, hq, d) or tuple(ks.shape) != (n, hkv, d)
+                    or tuple(vs.shape) != (n, hkv, d)):
+                raise ValueError(f"structured inputs do not match {wl.name}")
+        self.structured = structured
+        self.layers = len(structured)
+        self.prob = pa.Problem(seq_len=n, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                               block_size=wl.block_size, num_proxy_groups=wl.num_proxy_groups,
+                               stride=wl.stride, dtype="bf16")
+        self.bufs = pa.Buffers(self.prob)
+        dev, bf = "cuda", torch.bfloat16
+        self.kvb = torch.empty(pa.proxyattn_kv_blocked_size(self.prob), dtype=torch.uint8,
+                               device=dev)
+        self.qws = torch.empty(pa.proxyattn_blocked_workspace_size(self.prob), dtype=torch.uint8,
+                               device=dev)
+        self.q = torch.empty(n, hq, d, dtype=bf, device=dev)
+        self.k = torch.empty(n, hkv, d, dtype=bf, device=dev)
+        self.v = torch.empty(n, hkv, d, dtype=bf, device=dev)
+        g = torch.Generator(device=dev).manual_seed(seed)
+
+        def w(rows, cols):
+            return torch.randn(rows, cols, device=dev, dtype=bf, generator=g) * rows ** -0.5
+
+        self.weights = [(w(hidden, (hq + 2 * hkv) * d), w(hq * d, hidden), w(hidden, 2 * inter),
+                         w(inter, hidden)) for _ in range(self.layers)]
+        self.norm = [(torch.ones(hidden, device=dev, dtype=bf),
+                      torch.ones(hidden, device=dev, dtype=bf)) for _ in range(self.layers)]
+        inv = 1.0 / (rope_theta ** (torch.arange(0, d, 2, device=dev, dtype=torch.float32) / d))
+        ang = torch.arange(n, device=dev, dtype=torch.float32)[:, None] * inv[None, :]
+        self.cos = ang.cos().to(bf)[:, None, :]
+        self.sin = ang.sin().to(bf)[:, None, :]
+
+    def embed(self, seed: int = 1):
+        """A seeded N(0, 1) hidden state [N, hidden] (the embedding output)."""
+        g = self.torch.Generator(device="cuda").manual_seed(seed)
+        return self.torch.randn(self.n, self.hidden, device="cuda", dtype=self.torch.bfloat16,
+                                generator=g)
+
+    def _rms(self, t, w):
         tf = t.float()
-        return (tf * torch.rsqrt(tf.pow(2).mean(-1, keepdim=True) + 1e-5)).to(bf) * w
+        return (tf * self.torch.rsqrt(tf.pow(2).mean(-1, keepdim=True) + 1e-5)).to(t.dtype) * w
 
-    def rope(t, heads):
-        t = t.reshape(n, heads, d)
-        a, b = t[..., : d // 2], t[..., d // 2:]
-        return torch.cat((a * cos - b * sin, b * cos + a * sin), dim=-1)
+    def _rope(self, t, heads):
+        t = t.reshape(self.n, heads, self.d)
+        h = self.d // 2
+        a, b = t[..., :h], t[..., h:]
+        return self.torch.cat((a * self.cos - b * self.sin, b * self.cos + a * self.sin), dim=-1)
 
-    def layer():
-        h = rms(x, nrm1)
-        qkv = h @ w_qkv
-        rope(qkv[:, : hq * d], hq)
-        rope(qkv[:, hq * d:(hq + hkv) * d], hkv)
-        x2 = x + attn_out @ w_o
-        gu = rms(x2, nrm2) @ w_gu
-        a = torch.nn.functional.silu(gu[:, :inter]) * gu[:, inter:]
-        return x2 + a @ w_dn
+    def attention(self, dense: bool, st):
+        pa, prob, b, wl = self.pa, self.prob, self.bufs, self.wl
+        if dense:
+            pa.proxyattn_prepare_kv(prob, self.k, self.v, self.kvb, st)
+            pa.proxyattn_dense_prefill_blocked(prob, self.q, self.kvb, b.out, b.lse, self.qws, st)
+            return
+        pa.proxyattn_estimate(prob, self.q, self.k, b.logscore, b.mass, b.workspace, st)
+        pa.proxyattn_select_budget(prob, b.logscore, b.mass, wl.gamma, wl.min_budget_tokens,
+                                   b.head_count, b.block_count, b.block_index, st)
+        pa.proxyattn_prepare_kv(prob, self.k, self.v, self.kvb, st)
+        pa.proxyattn_block_sparse_prefill_blocked(prob, self.q, self.kvb, b.block_count,
+                                                  b.block_index, b.out, b.lse, self.qws, st)
 
-    layer()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        layer()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / reps
+    def layer(self, l: int, x, dense: bool, ev=None, hook=None):
+        """Layer l on hidden state x (not modified); returns the next hidden state.
+        `ev`: two events recorded around the attention; `hook(l)` runs right
+        after the attention is enqueued (tests read the layer's buffers there)."""
+        torch = self.torch
+        n, hq, hkv, d, a = self.n, self.hq, self.hkv, self.d, self.alpha
+        w_qkv, w_o, w_gu, w_dn = self.weights[l]
+        n1, n2 = self.norm[l]
+        qs, ks, vs = self.structured[l]
+        st = torch.cuda.current_stream()
+        qkv = self._rms(x, n1) @ w_qkv
+        torch.add(qs, self._rope(qkv[:, :hq * d], hq), alpha=a, out=self.q)
+        torch.add(ks, self._rope(qkv[:, hq * d:(hq + hkv) * d], hkv), alpha=a, out=self.k)
+        torch.add(vs.view(n, hkv * d), qkv[:, (hq + hkv) * d:], alpha=a,
+                  out=self.v.view(n, hkv * d))
+        del qkv
+        if ev:
+            ev[0].record(st)
+        self.attention(dense, st)
+        if ev:
+            ev[1].record(st)
+        if hook:
+            hook(l)
+        x = x + self.bufs.out.view(n, hq * d) @ w_o
+        gu = self._rms(x, n2) @ w_gu
+        act = torch.nn.functional.silu(gu[:, :self.inter]) * gu[:, self.inter:]
+        del gu
+        return x + act @ w_dn
+
+    def forward(self, x, dense: bool, timed: bool = False, hook=None):
+        """All layers on the embedding output x; returns (hidden state, times).
+        With `timed`, times = (total ms, attention ms summed over layers) from
+        HIP events on the current stream, one region around all layers."""
+        torch = self.torch
+        st = torch.cuda.current_stream()
+        evs = ([[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                for _ in range(self.layers)] if timed else [None] * self.layers)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if timed:
+            torch.cuda.synchronize()
+            t0.record(st)
+        for l in range(self.layers):
+            x = self.layer(l, x, dense, evs[l], hook)
+        if not timed:
+            return x, None
+        t1.record(st)
+        torch.cuda.synchronize()
+        return x, (t0.elapsed_time(t1), sum(e[0].elapsed_time(e[1]) for e in evs))
 
 
 def _stack_layer(job):
@@ -541,18 +631,11 @@ def _stack_layer(job):
     return seed, paths
 
 
-def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int, workers: int,
-              ttft: bool = False):
-    """A stack of `layers` layers of workload `wname`, layer l drawn with seed l.
-
-    Layers are generated by `workers` spawned processes (started before this
-    process touches the GPU), at most workers + 1 ahead of the GPU, and passed
-    through .npy files; each layer is timed like the default line (sparse path
-    and dense kernel), then the stack totals are printed.  With `ttft`, the
-    totals add the non-attention work of a Llama-3-8B-shaped decoder layer
-    (decoder_nonattn_ms, timed once at this length) to every layer: a
-    prefill time-to-first-token with the sparse path vs dense attention.
-    """
+def _layer_stream(wname: str, layers: int, workers: int):
+    """Yield (layer, (q, k, v) bf16 device tensors) for layers 0..layers-1 of
+    workload `wname`, layer l drawn with seed l by `workers` spawned processes
+    (started before this process touches the GPU), at most workers + 1 ahead
+    of the consumer, and passed through .npy files."""
     import multiprocessing as mp
     import shutil
     import tempfile
@@ -569,8 +652,6 @@ def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int
     outdir = tempfile.mkdtemp(prefix="proxyattn_stack_", dir=tmp_root)
     threads = max(1, (os.cpu_count() or workers) // workers)
     pool = mp.get_context("spawn").Pool(workers)
-    sums = {"t_total": 0.0, "t_est": 0.0, "t_sel": 0.0, "t_attn": 0.0, "t_dense": 0.0, "blocks": 0,
-            "causal": 0}
     try:
         import torch
         pending = {}
@@ -584,7 +665,7 @@ def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int
 
         fill()
         for layer in range(layers):
-            seed, paths = pending.pop(layer).get()
+            _, paths = pending.pop(layer).get()
             fill()
             bits = [np.load(p) for p in paths]
             for p in paths:
@@ -592,35 +673,37 @@ def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int
             inputs = tuple(torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
                            for a in bits)
             del bits
-            wl = base.replace(seed=seed)
-            res, _, _ = measure(wl, steps, warmup, dense_steps, with_dense=True, inputs=inputs)
-            del inputs
-            line = summary_line(wl, res, steps)
-            line["layer"] = layer
-            print(json.dumps(line), flush=True)
-            sums["t_total"] += res["ms_total"]
-            sums["t_est"] += res["t_est"]
-            sums["t_sel"] += res["t_sel"]
-            sums["t_attn"] += res["t_attn"]
-            sums["t_dense"] += res["t_dense"]
-            sums["blocks"] += res["total_blocks"]
-            mq = wl.num_blocks
-            sums["causal"] += wl.num_q_heads * mq * (mq + 1) // 2
-        t_other = decoder_nonattn_ms(base.seq_len) if ttft else None
+            yield layer, inputs
     finally:
         pool.terminate()
         pool.join()
         shutil.rmtree(outdir, ignore_errors=True)
+
+
+def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int, workers: int):
+    """The attention of a stack of `layers` layers of workload `wname`, layer
+    l drawn with seed l: each layer timed like the default line (sparse path
+    and dense kernel, one JSON line per layer), then the stack totals."""
+    from paper_2509_24745_amd.synth import WORKLOADS
+    base = WORKLOADS[wname]
+    sums = {"t_total": 0.0, "t_est": 0.0, "t_sel": 0.0, "t_attn": 0.0, "t_dense": 0.0, "blocks": 0,
+            "causal": 0}
+    for layer, inputs in _layer_stream(wname, layers, workers):
+        wl = base.replace(seed=layer)
+        res, _, _ = measure(wl, steps, warmup, dense_steps, with_dense=True, inputs=inputs)
+        del inputs
+        line = summary_line(wl, res, steps)
+        line["layer"] = layer
+        print(json.dumps(line), flush=True)
+        sums["t_total"] += res["ms_total"]
+        sums["t_est"] += res["t_est"]
+        sums["t_sel"] += res["t_sel"]
+        sums["t_attn"] += res["t_attn"]
+        sums["t_dense"] += res["t_dense"]
+        sums["blocks"] += res["total_blocks"]
+        mq = wl.num_blocks
+        sums["causal"] += wl.num_q_heads * mq * (mq + 1) // 2
     f_dense = layers * 4.0 * base.num_q_heads * base.head_dim * base.seq_len * (base.seq_len + 1) / 2
-    if ttft:
-        t_sp = sums["t_total"] + layers * t_other
-        t_dn = sums["t_dense"] + layers * t_other
-        print(json.dumps({
-            "ttft_stack": wname, "layers": layers, "nonattn_ms_per_layer": round(t_other, 3),
-            "ttft_sparse_ms": round(t_sp, 1), "ttft_dense_ms": round(t_dn, 1),
-            "ttft_speedup": round(t_dn / t_sp, 3),
-            "attention_share_dense": round(sums["t_dense"] / t_dn, 3),
-            "attention_share_sparse": round(sums["t_total"] / t_sp, 3)}), flush=True)
     print(json.dumps({
         "stack": wname, "layers": layers, "t_total_ms": round(sums["t_total"], 3),
         "t_estimate_ms": round(sums["t_est"], 3), "t_select_ms": round(sums["t_sel"], 3),
@@ -629,6 +712,59 @@ def run_stack(wname: str, layers: int, steps: int, warmup: int, dense_steps: int
         "dense_equiv_tflops": round(f_dense / (sums["t_total"] * 1e-3) / 1e12, 2),
         "estimation_overhead_pct": round(100.0 * (sums["t_est"] + sums["t_sel"]) / sums["t_total"], 2),
         "sparsity": round(1.0 - sums["blocks"] / sums["causal"], 4)}), flush=True)
+
+
+def run_decoder(wname: str, layers: int, workers: int, reps: int = 1):
+    """A `layers`-layer decoder prefill (DecoderPrefill) on workload `wname`'s
+    shape, layer l's structured inputs drawn with seed l: the whole prefill
+    timed as one region with the sparse path and again with the dense kernel,
+    from the same embedding output, `reps` times each (the last is reported)."""
+    import torch
+    from paper_2509_24745_amd.synth import WORKLOADS
+    base = WORKLOADS[wname]
+    structured = []
+    t = time.time()
+    for layer, inputs in _layer_stream(wname, layers, workers):
+        structured.append(inputs)
+        print(f"[bench] decoder layer {layer}: structured inputs resident "
+              f"({time.time() - t:.0f} s)", file=sys.stderr, flush=True)
+    dec = DecoderPrefill(base, structured)
+    x0 = dec.embed()
+    for dense in (False, True):                       # warm-up: layer 0 both ways
+        dec.layer(0, x0, dense)
+    torch.cuda.synchronize()
+    blocks = []
+
+    def count(_):
+        blocks.append(dec.bufs.block_count.sum())
+
+    for rep in range(reps):
+        blocks.clear()
+        xs, (t_sp, a_sp) = dec.forward(x0, dense=False, timed=True, hook=count)
+        print(f"[bench] decoder sparse prefill {t_sp:.1f} ms (attention {a_sp:.1f})",
+              file=sys.stderr, flush=True)
+        xd, (t_dn, a_dn) = dec.forward(x0, dense=True, timed=True)
+        print(f"[bench] decoder dense prefill {t_dn:.1f} ms (attention {a_dn:.1f})",
+              file=sys.stderr, flush=True)
+        if rep + 1 < reps:
+            del xs, xd
+    mq = base.num_blocks
+    causal = base.num_q_heads * mq * (mq + 1) // 2
+    sp = [1.0 - int(c) / causal for c in blocks]
+    diff = float((xs.float() - xd.float()).norm() / xd.float().norm())
+    print(json.dumps({
+        "ttft_decoder": wname, "layers": layers, "hidden": dec.hidden,
+        "intermediate": dec.inter, "alpha": dec.alpha,
+        "ttft_sparse_ms": round(t_sp, 1), "ttft_dense_ms": round(t_dn, 1),
+        "ttft_speedup": round(t_dn / t_sp, 3),
+        "attention_sparse_ms": round(a_sp, 1), "attention_dense_ms": round(a_dn, 1),
+        "attention_speedup": round(a_dn / a_sp, 3),
+        "nonattn_sparse_ms": round(t_sp - a_sp, 1), "nonattn_dense_ms": round(t_dn - a_dn, 1),
+        "attention_share_dense": round(a_dn / t_dn, 3),
+        "attention_share_sparse": round(a_sp / t_sp, 3),
+        "sparsity_mean": round(float(np.mean(sp)), 4),
+        "sparsity_min_max": [round(min(sp), 4), round(max(sp), 4)],
+        "final_hidden_rel_diff": round(diff, 5)}), flush=True)
 
 
 W128 = "llama3_8b_n131072"
@@ -824,9 +960,12 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n}))
         return
     from paper_2509_24745_amd.synth import WORKLOADS
+    if args.stack and args.ttft:
+        run_decoder(args.workload, args.stack, args.stack_workers)
+        return
     if args.stack:
         run_stack(args.workload, args.stack, args.steps, args.warmup, args.dense_steps,
-                  args.stack_workers, ttft=args.ttft)
+                  args.stack_workers)
         return
     if args.sweep:
         run_sweep(args.sweep, args.steps, args.warmup, args.dense_steps)

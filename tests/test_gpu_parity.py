@@ -621,19 +621,29 @@ def _sampled_rows_check(wl, nsample: int, pre: dict | None = None, pool=None):
     U = _gpu()
     from tests import pregen
     rows = pregen.sample_rows(wl.seq_len, nsample)
-    brows = np.unique(rows // wl.block_size)
-    sc = O.default_scale(wl.head_dim)
     if pre is None:
         q, k, v = U.inputs(wl)
+    else:
+        q, k, v = pre["q"], pre["k"], pre["v"]
+    gpu = U.run_path(U.problem_of(wl), q, k, v, wl.gamma, rows=rows)
+    check_sampled_rows(wl, rows, q, k, v, gpu, pre, pool)
+
+
+def check_sampled_rows(wl, rows, q, k, v, gpu: dict, pre: dict | None = None, pool=None):
+    """Check the path's results `gpu` on inputs q, k, v (host arrays) against
+    the oracle: pooled heads, every head's mass and budget, the scores and
+    lists of the block rows of `rows`, and the attention of `rows` (gpu's
+    out and lse hold those rows only).  `pre` and `pool` as in
+    _sampled_rows_check."""
+    brows = np.unique(np.asarray(rows) // wl.block_size)
+    sc = O.default_scale(wl.head_dim)
+    if pre is None:
         qg, kg = O.pool_proxy_heads(q, k, wl.num_proxy_groups, wl.stride, wl.dtype)
         oa, _ = O.proxy_block_logscore(qg, kg, wl.seq_len, wl.block_size, wl.stride, sc,
                                        rows=brows)
         mass = O.lastblock_mass(q, k, wl.block_size, sc)
     else:
-        q, k, v = pre["q"], pre["k"], pre["v"]
         qg, kg, oa, mass = pre["qg"], pre["kg"], pre["logA"], pre["mass"]
-    prob = U.problem_of(wl)
-    gpu = U.run_path(prob, q, k, v, wl.gamma, rows=rows)
     assert np.array_equal(gpu["qg"], qg) and np.array_equal(gpu["kg"], kg), "pooled heads differ"
     ga = gpu["logA"][:, brows]
     ob = oa[:, brows]
