@@ -18,6 +18,7 @@ sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -880,16 +881,17 @@ PAPER_CONTEXT = {
 }
 
 
-# (PROXYATTN_ATTN_ORDER, PROXYATTN_ATTN_CHUNK_ROWS) points of --work-orders:
-# 0 = longest rows first, heads fastest; 1 = chunks of R rows x all heads;
-# 2 = chunks of R rows x the query heads of one KV head, KV head by KV head.
-WORK_ORDERS = [(0, 1), (1, 2), (1, 8), (2, 1), (2, 4), (2, 16), (2, 64)]
+# (attn_order, attn_chunk_rows) points of --work-orders (problem descriptor
+# fields): 1 = longest rows first, heads fastest; 2 = chunks of R rows x all
+# heads; 3 = chunks of R rows x the query heads of one KV head, KV head by KV
+# head.
+WORK_ORDERS = [(1, 1), (2, 2), (2, 8), (3, 1), (3, 4), (3, 16), (3, 64)]
 
 
 def run_work_orders(wl, reps: int):
     """Time the block-sparse call on one set of lists under each work-item
-    order of the library (its PROXYATTN_ATTN_ORDER / PROXYATTN_ATTN_CHUNK_ROWS
-    settings), one JSON line per order.  Launch sequence, which a rocprofv3
+    order of the library (the problem's attn_order / attn_chunk_rows), one
+    JSON line per order.  Launch sequence, which a rocprofv3
     --pmc run of this mode sees in the same order: per order one untimed call,
     then `reps` timed calls."""
     import torch
@@ -909,34 +911,24 @@ def run_work_orders(wl, reps: int):
                                bufs.head_count, bufs.block_count, bufs.block_index, st)
     torch.cuda.synchronize()
     blocks = int(bufs.block_count.sum().item())
-    saved = {x: os.environ.get(x) for x in ("PROXYATTN_ATTN_ORDER", "PROXYATTN_ATTN_CHUNK_ROWS")}
-    try:
-        for order, rows in WORK_ORDERS:
-            os.environ["PROXYATTN_ATTN_ORDER"] = str(order)
-            os.environ["PROXYATTN_ATTN_CHUNK_ROWS"] = str(rows)
-            call = lambda: pa.proxyattn_block_sparse_prefill(
-                prob, q, k, v, bufs.block_count, bufs.block_index, bufs.out, None,
-                bufs.workspace, st)
+    for order, rows in WORK_ORDERS:
+        po = dataclasses.replace(prob, attn_order=order, attn_chunk_rows=rows)
+        call = lambda: pa.proxyattn_block_sparse_prefill(
+            po, q, k, v, bufs.block_count, bufs.block_index, bufs.out, None, bufs.workspace, st)
+        call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
             call()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(st)
-            for _ in range(reps):
-                call()
-            e1.record(st)
-            torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1) / reps
-            print(json.dumps({"workload": wl.name, "attn_order": order, "chunk_rows": rows,
-                              "attn_ms": round(ms, 3), "reps": reps, "computed_blocks": blocks,
-                              "attn_tflops": round(4.0 * wl.block_size ** 2 * wl.head_dim *
-                                                   blocks / (ms * 1e-3) / 1e12, 1)}),
-                  flush=True)
-    finally:
-        for x, val in saved.items():
-            if val is None:
-                os.environ.pop(x, None)
-            else:
-                os.environ[x] = val
+        e1.record(st)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        print(json.dumps({"workload": wl.name, "attn_order": order, "chunk_rows": rows,
+                          "attn_ms": round(ms, 3), "reps": reps, "computed_blocks": blocks,
+                          "attn_tflops": round(4.0 * wl.block_size ** 2 * wl.head_dim *
+                                               blocks / (ms * 1e-3) / 1e12, 1)}),
+              flush=True)
 
 
 def main():

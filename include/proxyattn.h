@@ -41,15 +41,6 @@
  *  - Results are bitwise deterministic (no floating-point atomics).
  *  - N == 0 is a valid empty problem: nothing is enqueued.
  *  - Inputs must be finite; non-finite inputs give unspecified outputs.
- *  - Two environment variables tune the order in which the attention kernel
- *    takes its work items; results are bitwise the same under every setting.
- *    PROXYATTN_ATTN_ORDER: 0 (longest block rows first, heads fastest),
- *    1 (chunks of R block rows x all heads) or 2 (chunks of R block rows x
- *    the query heads of one KV head, KV head by KV head).
- *    PROXYATTN_ATTN_CHUNK_ROWS: R, an integer in [1, 8192].
- *    Unset or empty selects the default, chosen by problem size.  Any other
- *    value makes every call that takes a problem descriptor fail with
- *    PROXYATTN_E_INVALID.
  */
 #ifndef PROXYATTN_H
 #define PROXYATTN_H
@@ -97,6 +88,15 @@ typedef struct proxyattn_problem {
     int64_t q_tok_stride, q_head_stride;
     int64_t kv_tok_stride, kv_head_stride; /* shared by K and V */
     int64_t o_tok_stride, o_head_stride;
+    /* Order in which the attention kernel takes its work items (a tuning
+     * knob: results are bitwise the same under every setting).
+     * attn_order: 0 selects by problem size; 1 longest block rows first,
+     * heads fastest; 2 chunks of R block rows x all query heads; 3 chunks of
+     * R block rows x the query heads of one KV head, KV head by KV head.
+     * attn_chunk_rows: R in [1, 8192]; 0 selects by problem size.  Values
+     * outside these ranges make every call fail with PROXYATTN_E_INVALID. */
+    int32_t attn_order;
+    int32_t attn_chunk_rows;
 } proxyattn_problem;
 
 /*

@@ -3,8 +3,6 @@
 // arguments before enqueuing anything, never allocates and never
 // synchronises.
 #include <algorithm>
-#include <errno.h>
-#include <limits.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -34,18 +32,6 @@ static int hip_fail(hipError_t e, const char* where) {
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-// Integer value of environment variable `name`: `dflt` when it is unset or
-// empty, INT_MIN when it is not a whole decimal integer in int range.
-static int env_int(const char* name, int dflt) {
-    const char* v = getenv(name);
-    if (!v || !*v) return dflt;
-    errno = 0;
-    char* end = nullptr;
-    const long x = strtol(v, &end, 10);
-    if (errno || end == v || *end || x < INT_MIN + 1 || x > INT_MAX) return INT_MIN;
-    return (int)x;
-}
 
 // Validates the descriptor and resolves it into a Shape.
 static int resolve(const proxyattn_problem* p, Shape* sh) {
@@ -129,20 +115,23 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     s.o_tok = p->o_tok_stride ? p->o_tok_stride : (int64_t)p->num_q_heads * d;
     s.o_head = p->o_head_stride ? p->o_head_stride : d;
     // attention work order (tuning knob).  Default: when the re-blocked K/V
-    // is larger than the MALL, KV-head-major chunks of 4 rows, so that the
+    // takes more than 3/4 of the MALL (which the queries, lists and outputs
+    // stream through as well), KV-head-major chunks of 4 rows, so that the
     // whole GPU works on one KV head's K/V at a time and it stays in the MALL
-    // (measured -3 % at 128K, -10 % at 256K); otherwise row chunks of 2 rows,
-    // which balance better (order 2 is ~10 % slower at 8K and equal at 32K).
+    // (measured -2 % at 64K, -3 % at 128K, -10 % at 256K with 8 KV heads);
+    // otherwise row chunks of 2 rows, which balance better (KV-head-major is
+    // ~5 % slower at 8K and 1 % at 32K).
     {
-        const size_t kvb_bytes = (size_t)s.hkv * s.mq * 2 * s.b * s.d * esz;
-        const bool big = kvb_bytes > kMallBytes;
-        s.attn_order = env_int("PROXYATTN_ATTN_ORDER", big ? 2 : 1);
-        s.attn_chunk_rows = env_int("PROXYATTN_ATTN_CHUNK_ROWS", big ? 4 : 2);
         // the item arithmetic multiplies R by head counts in int
-        if (s.attn_order < 0 || s.attn_order > 2)
-            return fail(PROXYATTN_E_INVALID, "PROXYATTN_ATTN_ORDER must be 0, 1 or 2");
-        if (s.attn_chunk_rows < 1 || s.attn_chunk_rows > 8192)
-            return fail(PROXYATTN_E_INVALID, "PROXYATTN_ATTN_CHUNK_ROWS must be an integer in [1, 8192]");
+        if (p->attn_order < 0 || p->attn_order > 3)
+            return fail(PROXYATTN_E_INVALID, "attn_order %d not in [0, 3]", p->attn_order);
+        if (p->attn_chunk_rows < 0 || p->attn_chunk_rows > 8192)
+            return fail(PROXYATTN_E_INVALID, "attn_chunk_rows %d not in [0, 8192]",
+                        p->attn_chunk_rows);
+        const size_t kvb_bytes = (size_t)s.hkv * s.mq * 2 * s.b * s.d * esz;
+        const bool big = kvb_bytes * 4 > kMallBytes * 3;
+        s.attn_order = p->attn_order ? p->attn_order - 1 : (big ? 2 : 1);
+        s.attn_chunk_rows = p->attn_chunk_rows ? p->attn_chunk_rows : (big ? 4 : 2);
     }
     const int64_t strides[6] = {s.q_tok, s.q_head, s.kv_tok, s.kv_head, s.o_tok, s.o_head};
     for (int j = 0; j < 6; ++j) {

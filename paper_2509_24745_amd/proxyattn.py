@@ -46,6 +46,8 @@ class proxyattn_problem(ctypes.Structure):
         ("kv_head_stride", ctypes.c_int64),
         ("o_tok_stride", ctypes.c_int64),
         ("o_head_stride", ctypes.c_int64),
+        ("attn_order", ctypes.c_int32),
+        ("attn_chunk_rows", ctypes.c_int32),
     ]
 
 
@@ -138,6 +140,8 @@ class Problem:
     kv_head_stride: int = 0
     o_tok_stride: int = 0
     o_head_stride: int = 0
+    attn_order: int = 0        # 0 by size; 1 plain, 2 row chunks, 3 KV-head-major chunks
+    attn_chunk_rows: int = 0   # 0 by size
 
     @property
     def num_blocks(self) -> int:
@@ -166,6 +170,7 @@ class Problem:
         p.q_tok_stride, p.q_head_stride = self.q_tok_stride, self.q_head_stride
         p.kv_tok_stride, p.kv_head_stride = self.kv_tok_stride, self.kv_head_stride
         p.o_tok_stride, p.o_head_stride = self.o_tok_stride, self.o_head_stride
+        p.attn_order, p.attn_chunk_rows = self.attn_order, self.attn_chunk_rows
         return p
 
 

@@ -92,24 +92,33 @@ def test_problem_validation(kw, code):
 
 
 @pytest.mark.parametrize("order,rows,ok", [
-    ("0", "1", True), ("1", "2", True), ("2", "8192", True), ("", "", True),
-    ("3", "4", False), ("-1", "4", False), ("2", "0", False), ("2", "-4", False),
-    ("2", "8193", False), ("2", "99999999999", False), ("2x", "4", False), ("2", "4.5", False),
+    (0, 0, True), (1, 1, True), (2, 2, True), (3, 8192, True), (0, 7, True), (3, 0, True),
+    (4, 4, False), (-1, 4, False), (3, -4, False), (3, 8193, False), (2**31 - 1, 4, False),
+    (3, -2**31, False),
 ])
-def test_work_order_settings_are_validated(order, rows, ok, monkeypatch):
-    """The attention work-order knobs reach kernel index arithmetic: values
-    outside the documented ranges, or not integers, fail every call with
-    E_INVALID before anything is enqueued."""
+def test_work_order_fields_are_validated(order, rows, ok):
+    """The attention work-order fields of the problem descriptor reach kernel
+    index arithmetic: values outside the documented ranges fail every call
+    with E_INVALID before anything is enqueued."""
     _lib()
-    monkeypatch.setenv("PROXYATTN_ATTN_ORDER", order)
-    monkeypatch.setenv("PROXYATTN_ATTN_CHUNK_ROWS", rows)
+    prob = _prob(attn_order=order, attn_chunk_rows=rows)
     if ok:
-        assert pa.proxyattn_workspace_size(_prob()) > 0
+        assert pa.proxyattn_workspace_size(prob) > 0
         return
     with pytest.raises(pa.ProxyAttnError) as ei:
-        pa.proxyattn_workspace_size(_prob())
+        pa.proxyattn_workspace_size(prob)
     assert ei.value.code == pa.E_INVALID
-    assert "PROXYATTN_ATTN_" in str(ei.value)
+    assert "attn_" in str(ei.value)
+
+
+def test_library_reads_no_environment(monkeypatch):
+    """Settings once read from the environment are descriptor fields now: the
+    old variables, even malformed, change nothing."""
+    _lib()
+    want = pa.proxyattn_workspace_size(_prob())
+    monkeypatch.setenv("PROXYATTN_ATTN_ORDER", "7x")
+    monkeypatch.setenv("PROXYATTN_ATTN_CHUNK_ROWS", "-1")
+    assert pa.proxyattn_workspace_size(_prob()) == want
 
 
 def test_bad_struct_size_and_null_problem():

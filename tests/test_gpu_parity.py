@@ -21,6 +21,7 @@ Bars (the parity tolerances, see oracle/check.py):
     2^-8 relative of the exact value, so |dlse| <= ln(1 + 2^-8) = 3.9e-3
     (reached when one key dominates a row); LSE_TOL = 4e-3.
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -354,7 +355,7 @@ def test_deterministic_across_runs_and_streams():
 
 @pytest.mark.parametrize("wl", [LLAMA.replace(seq_len=4096 + 77), QWEN.replace(seq_len=3000)],
                          ids=["llama_n4173", "qwen_n3000"])
-def test_work_orders_give_identical_output(wl, monkeypatch):
+def test_work_orders_give_identical_output(wl):
     """Every work order and chunk size must hand each (head, block row) item to
     exactly one workgroup, which computes it alone: sparse and dense outputs
     and lse are then bitwise those of the default order (ragged N, GQA 4 and
@@ -367,23 +368,22 @@ def test_work_orders_give_identical_output(wl, monkeypatch):
     b = pa.prefill(prob, qd, kd, vd, wl.gamma)
     torch.cuda.synchronize()
 
-    def run(dense):
+    def run(p, dense):
         out = torch.full_like(b.out, float("nan"))
         lse = torch.full_like(b.lse, float("nan"))
         if dense:
-            pa.proxyattn_dense_prefill(prob, qd, kd, vd, out, lse, b.workspace)
+            pa.proxyattn_dense_prefill(p, qd, kd, vd, out, lse, b.workspace)
         else:
-            pa.proxyattn_block_sparse_prefill(prob, qd, kd, vd, b.block_count, b.block_index,
+            pa.proxyattn_block_sparse_prefill(p, qd, kd, vd, b.block_count, b.block_index,
                                               out, lse, b.workspace)
         torch.cuda.synchronize()
         return out.cpu(), lse.cpu()
 
-    ref = {dense: run(dense) for dense in (False, True)}
-    for order, rows in ((0, 1), (1, 1), (1, 3), (2, 1), (2, 4), (2, 7)):
-        monkeypatch.setenv("PROXYATTN_ATTN_ORDER", str(order))
-        monkeypatch.setenv("PROXYATTN_ATTN_CHUNK_ROWS", str(rows))
+    ref = {dense: run(prob, dense) for dense in (False, True)}
+    for order, rows in ((1, 1), (2, 1), (2, 3), (3, 1), (3, 4), (3, 7), (0, 5)):
+        p = dataclasses.replace(prob, attn_order=order, attn_chunk_rows=rows)
         for dense in (False, True):
-            out, lse = run(dense)
+            out, lse = run(p, dense)
             assert torch.equal(out, ref[dense][0]), (order, rows, dense)
             assert torch.equal(lse, ref[dense][1]), (order, rows, dense)
 
