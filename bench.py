@@ -181,6 +181,9 @@ def _kernel_label(name: str) -> str:
     import re
     m = re.match(r"_ZN2pa\d+(\w+?)I(DF16b|f)Li(\d+)E(?:Li(\d+)E)?(?:Lb([01])E)?", name)
     if not m:
+        m2 = re.match(r"_ZN2pa\d+(\w+?)ILi(\d+)EE", name)   # one integer parameter
+        if m2:
+            return f"{m2.group(1)}<{m2.group(2)}>"
         return name.split("(")[0][:48]
     kind, t, a, b, flag = m.groups()
     t = "bf16" if t == "DF16b" else "f32"
