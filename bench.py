@@ -867,7 +867,12 @@ def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
             variant = "static"
             static_k = max(1, int(round(last_mean[(key, wl.gamma, wl.min_budget_tokens)])))
         d = dense.get(key)
-        res, host, inputs = measure(wl, steps, warmup, dense_steps, with_dense=d is None,
+        # shorter sequences take more steps, so that every point's timed
+        # region is about as long as the 128K point's (host launch latency
+        # and clock ramp-up otherwise show in a region of a few milliseconds)
+        n_steps = min(1000, max(steps, int(steps * (131072 / wl.seq_len) ** 2)))
+        n_dense = min(200, max(dense_steps, int(dense_steps * (131072 / wl.seq_len) ** 2)))
+        res, host, inputs = measure(wl, n_steps, warmup, n_dense, with_dense=d is None,
                                     inputs=cache.get(key), variant=variant, static_k=static_k,
                                     dense_lse=d["lse"] if d else None)
         cache = {key: inputs}
@@ -878,7 +883,7 @@ def run_sweep(name: str, steps: int, warmup: int, dense_steps: int):
             res["t_dense"], res["dense_mfma_frac"] = d["t"], d["frac"]
         if variant == "dynamic":
             last_mean[(key, wl.gamma, wl.min_budget_tokens)] = res["head_count_mean"]
-        line = summary_line(wl, res, steps)
+        line = summary_line(wl, res, n_steps)
         if with_overlap:
             line["head_overlap_top1024"] = overlap_stats(wl, inputs)
         print(json.dumps(line), flush=True)
