@@ -564,6 +564,12 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
 #pragma unroll
             for (int j = 0; j < kReadLead; ++j) f[j] = frag(j);
             __builtin_amdgcn_sched_barrier(0);
+            // While a wave issues its MFMA pipeline it takes precedence over
+            // the other workgroup's wave on the same SIMD when that one is at
+            // its step boundary (copy wait, barrier, copy issue, rescale
+            // check), so the matrix pipe is fed first: -0.5 to -0.7 % of the
+            // attention time at 32K and 128K against equal priorities.
+            __builtin_amdgcn_s_setprio(3);
 #pragma unroll
             for (int j = 0; j < NF; ++j) {
                 if (j < NQ) {
@@ -599,6 +605,7 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
+            __builtin_amdgcn_s_setprio(0);
         } else {
             qk(sn, slot.k((st + 1) & 1));
 #pragma unroll
