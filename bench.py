@@ -52,11 +52,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=24,
                     help="block rows of the oracle sample (all heads)")
-    ap.add_argument("--sweep", choices=["gamma_sigma_128k", "llama_32k", "qwen_64k",
-                                         "llama_256k_layer", "budget_variants_128k",
-                                         "stride_128k", "min_budget_128k", "groups_128k",
-                                         "head_similarity_128k", "seq_len_llama"],
-                    default=None,
+    ap.add_argument("--sweep", choices=sorted(SWEEPS), default=None,
                     help="print one JSON line per point of a workload sweep instead")
     ap.add_argument("--work-orders", action="store_true",
                     help="time the sparse attention call of --workload under each work-item "
@@ -68,6 +64,9 @@ def parse():
                     help="with --stack: run a LAYERS-layer decoder prefill around the path "
                          "(projections, RoPE, MLP; one timed region) and report the "
                          "time-to-first-token with the sparse path vs the dense kernel")
+    ap.add_argument("--shard", type=int, default=None, metavar="P",
+                    help="time --workload with one proxy group per KV head, whole and in P "
+                         "head shards (each as one of P GPUs would run it); one JSON line")
     ap.add_argument("--stack-workers", type=int, default=4,
                     help="processes generating stack layers ahead of the GPU")
     ap.add_argument("--profile-summary", metavar="DIR", default=None,
@@ -813,6 +812,45 @@ SWEEPS = {
 }
 
 
+def run_shard(wname: str, parts: int, steps: int, warmup: int, dense_steps: int):
+    """Head sharding, timed on one GPU: the layer of workload `wname` with one
+    proxy group per KV head (G = Hkv), whole and in `parts` parts of Hq/P
+    query heads and Hkv/P KV heads.  Each part runs the path on its own
+    slices of Q, K and V, as one of P GPUs would, with no data from the
+    others (the part's results are those heads' results of the whole layer;
+    tests/test_gpu_shard.py checks that).  Prints one JSON line: the whole
+    step, every part's step, and the parallel efficiency the slowest part
+    allows, (whole / P) / slowest part."""
+    from paper_2509_24745_amd.synth import WORKLOADS
+    base = WORKLOADS[wname]
+    if parts < 1 or base.num_kv_heads % parts:
+        raise SystemExit(f"--shard: the parts must divide the {base.num_kv_heads} KV heads")
+    wl = base.replace(num_proxy_groups=base.num_kv_heads)
+    full, _, (q, k, v) = measure(wl, steps, warmup, dense_steps, with_dense=True)
+    rq, rk, rg = wl.num_q_heads // parts, wl.num_kv_heads // parts, wl.num_proxy_groups // parts
+    res = []
+    for s in range(parts):
+        sl = (q[:, s * rq:(s + 1) * rq].contiguous(), k[:, s * rk:(s + 1) * rk].contiguous(),
+              v[:, s * rk:(s + 1) * rk].contiguous())
+        ws = wl.replace(num_q_heads=rq, num_kv_heads=rk, num_proxy_groups=rg,
+                        name=f"{wl.name}_part{s}of{parts}")
+        r, _, _ = measure(ws, steps, warmup, dense_steps, with_dense=False, inputs=sl)
+        res.append(r)
+        del sl
+    t_parts = [r["ms_total"] for r in res]
+    print(json.dumps({
+        "shard": wl.name, "parts": parts, "num_proxy_groups": wl.num_proxy_groups,
+        "part_heads": [rq, rk, rg], "t_whole_ms": round(full["ms_total"], 3),
+        "t_part_ms": [round(t, 3) for t in t_parts], "t_part_max_ms": round(max(t_parts), 3),
+        "t_whole_over_parts_ms": round(full["ms_total"] / parts, 3),
+        "parallel_efficiency": round(full["ms_total"] / parts / max(t_parts), 3),
+        "t_dense_whole_ms": round(full["t_dense"], 3),
+        "speedup_vs_dense_sharded": round(full["t_dense"] / parts / max(t_parts), 3),
+        "sparsity_whole": round(full["sparsity"], 4),
+        "sparsity_parts": [round(r["sparsity"], 4) for r in res],
+        "attn_mfma_frac_parts": [round(r["achieved"] / r["peak"], 4) for r in res]}), flush=True)
+
+
 def overlap_stats(wl, inputs, topk: int = 1024):
     """Eq. 4 overlap matrices of the last query token on the GPU, summarised:
     mean over pairs of different heads, split into pairs sharing a KV head
@@ -972,6 +1010,9 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n}))
         return
     from paper_2509_24745_amd.synth import WORKLOADS
+    if args.shard:
+        run_shard(args.workload, args.shard, args.steps, args.warmup, args.dense_steps)
+        return
     if args.stack and args.ttft:
         run_decoder(args.workload, args.stack, args.stack_workers)
         return

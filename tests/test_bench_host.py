@@ -28,7 +28,7 @@ def test_sweeps_are_well_formed_and_selectable():
             wl = WORKLOADS[wname].replace(**kw) if kw else WORKLOADS[wname]
             assert wl.num_q_heads % wl.num_proxy_groups == 0
             assert variant.replace("+overlap", "") in ("dynamic", "row_ratio", "static_match")
-    for fn in ("measure", "run_sweep", "run_stack", "_stack_layer", "_layer_stream", "run_decoder",
+    for fn in ("measure", "run_sweep", "run_stack", "_stack_layer", "_layer_stream", "run_decoder", "run_shard",
                "DecoderPrefill",
                "overlap_stats", "cpu_baseline", "profile_summary"):
         assert callable(getattr(bench, fn)), fn
