@@ -40,7 +40,9 @@ Readings of passages the paper leaves open:
   * the budget uses each head's own Q and K at full resolution, the last
     min(b, N) query tokens, causal.
   * "avgpool" sums the last-block probabilities over the rows and over the
-    keys of each key block (mean vs. sum cancels in the normalisation).
+    keys of each key block: with b keys in every block, mean and sum differ
+    by one factor that the normalisation cancels; a partial last key block
+    (N not a multiple of b) keeps its sum, the probability it receives.
   * sort is descending; the budget is k*+1 blocks where k* is the first
     0-based prefix index whose cumulative mass reaches gamma (N_k if none,
     and N_k whenever gamma >= 1), then raised to ceil(min_budget/b) and
