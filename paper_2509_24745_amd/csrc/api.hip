@@ -292,9 +292,9 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
     const int64_t min_blocks64 = ((int64_t)min_budget_tokens + sh.b - 1) / sh.b;
     const int min_blocks = (int)(min_blocks64 > sh.mq ? sh.mq : min_blocks64);
     hipStream_t st = (hipStream_t)stream;
-    PA_LAUNCH(launch_budget(sh, lastblk_mass, gamma, min_blocks, head_count, st), "budget");
-    PA_LAUNCH(launch_select(sh, block_logscore, head_count, 0, 0, block_count, block_index, st),
-              "select");
+    PA_LAUNCH(launch_budget_select(sh, lastblk_mass, gamma, min_blocks, head_count, block_logscore,
+                                   block_count, block_index, st),
+              "budget_select");
     return PROXYATTN_OK;
 }
 

@@ -129,17 +129,32 @@ __device__ __forceinline__ void pool_body(const Shape& sh, const T* __restrict__
     float aq[V], ak[V];
 #pragma unroll
     for (int e = 0; e < V; ++e) { aq[e] = 0.f; ak[e] = 0.f; }
-    for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
-        const T* qp = q + t * sh.q_tok + (int64_t)i * sh.q_head + slice * V;
-        const T* kp = k + t * sh.kv_tok + (int64_t)(i / sh.rep) * sh.kv_head + slice * V;
-        const uint4 qv = *reinterpret_cast<const uint4*>(qp);
-        const uint4 kv = *reinterpret_cast<const uint4*>(kp);
-        const T* qe = reinterpret_cast<const T*>(&qv);
-        const T* ke = reinterpret_cast<const T*>(&kv);
+    // the heads' slices are loaded kPoolBatch at a time (all in flight
+    // together; a batch past the group's last head re-reads that head and
+    // discards it), then added in ascending head order
+    constexpr int kPoolBatch = 4;
+    const int i0 = g * sh.gsize, i1 = i0 + sh.gsize;
+    for (int ib = i0; ib < i1; ib += kPoolBatch) {
+        uint4 qv[kPoolBatch], kv[kPoolBatch];
 #pragma unroll
-        for (int e = 0; e < V; ++e) {
-            aq[e] = aq[e] + to_f32<T>(qe[e]);
-            ak[e] = ak[e] + to_f32<T>(ke[e]);
+        for (int u = 0; u < kPoolBatch; ++u) {
+            const int i = min(ib + u, i1 - 1);
+            qv[u] = *reinterpret_cast<const uint4*>(q + t * sh.q_tok + (int64_t)i * sh.q_head +
+                                                    slice * V);
+            kv[u] = *reinterpret_cast<const uint4*>(k + t * sh.kv_tok +
+                                                    (int64_t)(i / sh.rep) * sh.kv_head + slice * V);
+        }
+#pragma unroll
+        for (int u = 0; u < kPoolBatch; ++u) {
+            if (ib + u < i1) {
+                const T* qe = reinterpret_cast<const T*>(&qv[u]);
+                const T* ke = reinterpret_cast<const T*>(&kv[u]);
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    aq[e] = aq[e] + to_f32<T>(qe[e]);
+                    ak[e] = ak[e] + to_f32<T>(ke[e]);
+                }
+            }
         }
     }
     uint4 oq, ok;
@@ -279,17 +294,37 @@ __device__ __forceinline__ void est_reduce_body(const Shape& sh, const float* __
     // the block's rows lie in one 128-row band of est_rowmax (BP divides
     // 128), which wrote chunks 0 .. nck-1 for them
     const int nck = (min((r0 / 128) * 128 + 127, sh.np - 1) / 32) / sh.est_kc + 1;
+    // the chunk pairs are read kChunkBatch at a time, all in flight together
+    // (a batch past the last chunk re-reads it: the max is unchanged and the
+    // sum skips it); the sum runs over the chunks in increasing order
+    constexpr int kChunkBatch = 8;
     for (int j = tid; j < BP; j += 256) {
         float v = 0.f;
         if (j < nr) {
             const float2* pp = rowpart + (int64_t)g * sh.est_nc * sh.np + r0 + j;
             float mx = kNegInf;
-            for (int cc = 0; cc < nck; ++cc) mx = fmaxf(mx, pp[(int64_t)cc * sh.np].x);
+            for (int c0 = 0; c0 < nck; c0 += kChunkBatch) {
+                float xs[kChunkBatch];
+#pragma unroll
+                for (int u = 0; u < kChunkBatch; ++u)
+                    xs[u] = pp[(int64_t)min(c0 + u, nck - 1) * sh.np].x;
+#pragma unroll
+                for (int u = 0; u < kChunkBatch; ++u) mx = fmaxf(mx, xs[u]);
+            }
             // mx is finite: key 0 (chunk 0) is visible to every row
             float sum = 0.f;
-            for (int cc = 0; cc < nck; ++cc) {
-                const float2 x = pp[(int64_t)cc * sh.np];
-                if (x.x != kNegInf) sum += x.y * fast_exp2(x.x - mx);
+            for (int c0 = 0; c0 < nck; c0 += kChunkBatch) {
+                float2 xs[kChunkBatch];
+#pragma unroll
+                for (int u = 0; u < kChunkBatch; ++u)
+                    xs[u] = pp[(int64_t)min(c0 + u, nck - 1) * sh.np];
+#pragma unroll
+                for (int u = 0; u < kChunkBatch; ++u) {
+                    // a select, not a branch, so that both halves of the
+                    // pair are loaded with the one 8-byte load
+                    const bool use = c0 + u < nck && xs[u].x != kNegInf;
+                    sum = use ? fmaf(xs[u].y, fast_exp2(xs[u].x - mx), sum) : sum;
+                }
             }
             v = mx + log2f(sum);
         }
@@ -415,13 +450,26 @@ __device__ __forceinline__ void mass_norm_body(const Shape& sh, const float2* __
     if (r >= nrows) return;   // whole waves; no barrier follows
     const int nmax = (t0 + r) / b;
     const float2* pr = part + ((int64_t)i * b + r) * mq;
+    // a lane's blocks nb = lane, lane + 64, ... in increasing order, read
+    // kNormBatch at a time (all in flight together); selects, not branches,
+    // so that each pair is one 8-byte load
+    constexpr int kNormBatch = 4;
     float m = kNegInf, s = 0.f;
-    for (int nb = lane; nb <= nmax; nb += 64) {
-        const float2 x = pr[nb];
-        if (x.x != kNegInf) {
+    for (int nb0 = lane; nb0 <= nmax; nb0 += 64 * kNormBatch) {
+        float2 xs[kNormBatch];
+#pragma unroll
+        for (int u = 0; u < kNormBatch; ++u) {
+            const int nb = nb0 + 64 * u;
+            xs[u] = pr[min(nb, nmax)];
+        }
+#pragma unroll
+        for (int u = 0; u < kNormBatch; ++u) {
+            const float2 x = xs[u];
+            const bool use = nb0 + 64 * u <= nmax && x.x != kNegInf;
             const float mn = fmaxf(m, x.x);
-            s = (m == kNegInf ? 0.f : s * fast_exp2(m - mn)) + x.y * fast_exp2(x.x - mn);
-            m = mn;
+            const float sn = (m == kNegInf ? 0.f : s * fast_exp2(m - mn)) + x.y * fast_exp2(x.x - mn);
+            s = use ? sn : s;
+            m = use ? mn : m;
         }
     }
     const float M = wave_max(m);   // finite: block 0 is visible to every row
@@ -447,17 +495,26 @@ __device__ __forceinline__ void mass_sum_body(const Shape& sh, const float2* __r
     __syncthreads();
     const float2* base = part + (int64_t)i * b * mq;
     const int nb = chunk * 64 + lane;
+    // a partial's rows (at most 128 / kMassPartials) are read together, all
+    // in flight at once, then accumulated (one fma each) in increasing order;
+    // an invisible block or a row past the last reads as (-inf, 0) and is
+    // skipped (a select, not a branch, so that each pair is one 8-byte load)
+    constexpr int kRowsPerPartial = 128 / kMassPartials;
 #pragma unroll
     for (int pp = 0; pp < kMassPartials / 4; ++pp) {
         const int p = w + 4 * pp;
+        float2 xs[kRowsPerPartial];
+#pragma unroll
+        for (int u = 0; u < kRowsPerPartial; ++u) {
+            const int r = p + kMassPartials * u;
+            xs[u] = (nb < mq && r < nrows && nb * b <= t0 + r) ? base[(int64_t)r * mq + nb]
+                                                              : make_float2(kNegInf, 0.f);
+        }
         float acc = 0.f;
-        if (nb < mq) {
-            for (int r = p; r < nrows; r += kMassPartials) {
-                if (nb * b <= t0 + r) {
-                    const float2 x = base[(int64_t)r * mq + nb];
-                    if (x.x != kNegInf) acc += x.y * fast_exp2(x.x - L[r]);
-                }
-            }
+#pragma unroll
+        for (int u = 0; u < kRowsPerPartial; ++u) {
+            const int r = min(p + kMassPartials * u, nrows - 1);
+            acc = xs[u].x != kNegInf ? fmaf(xs[u].y, fast_exp2(xs[u].x - L[r]), acc) : acc;
         }
         ps[p][lane] = acc;
     }

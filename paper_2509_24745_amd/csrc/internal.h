@@ -118,6 +118,11 @@ hipError_t launch_budget(const Shape& sh, const float* mass, float gamma, int mi
 hipError_t launch_select(const Shape& sh, const float* logA, const int* head_count,
                          int row_ratio, int ascending, int* block_count, int* block_index,
                          hipStream_t st);
+// launch_budget then launch_select (rank order, constant K), as one launch
+// when Nk <= 64; the counts and lists are the same either way.
+hipError_t launch_budget_select(const Shape& sh, const float* mass, float gamma, int min_blocks,
+                                int* head_count, const float* logA, int* block_count,
+                                int* block_index, hipStream_t st);
 hipError_t launch_check_lists(const Shape& sh, const int* block_count, const int* block_index,
                               int* status, hipStream_t st);
 // launch_kv_block also resets the attention work queues when `queue` is not

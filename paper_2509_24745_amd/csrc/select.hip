@@ -18,6 +18,17 @@
 //   together in time are shared through the L2.  On request the same sets
 //   are listed by ascending block index instead (a rank table in LDS and a
 //   stream compaction per head).
+// budget + select in one launch (Nk <= 64, rank order): in every select
+//   workgroup, wave 0 sorts the row's candidates in registers (one per
+//   lane) while waves 1-3 derive the budgets of the group's heads, three
+//   heads at a time per wave with one block per lane, by the budget
+//   workgroup's own arithmetic (the same sums in the same order, the same
+//   sorting network over the same padded shares, the same prefix sums), so
+//   the counts and lists are those of the two launches for masses without
+//   NaN; the workgroups of block row 0 write the counts out.  Lane
+//   exchanges go through DPP where the pattern allows.  On short sequences
+//   the second launch, its dependent wait and the LDS sort's barriers are
+//   most of the selection time.
 // check_lists: one workgroup per (block row m, head i); validates a
 //   caller-made list against what the attention step accepts.
 #include "common.h"
@@ -121,15 +132,149 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(Shape sh,
     }
 }
 
+// Lane exchange x[l ^ O] for a compile-time O: DPP for O < 16 (quad
+// permutations; O = 4 as the quad reversal followed by the half-row mirror,
+// since (7 - l) ^ 3 = l ^ 4 within 8 lanes; O = 8 as the row rotation by 8),
+// an LDS permute for 16, v_permlane32_swap for 32.
+template <int O>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t x) {
+    if constexpr (O == 1) {
+        return __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+    } else if constexpr (O == 2) {
+        return __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+    } else if constexpr (O == 4) {
+        const uint32_t y = __builtin_amdgcn_update_dpp(0, x, 0x1B, 0xF, 0xF, false);  // [3,2,1,0]
+        return __builtin_amdgcn_update_dpp(0, y, 0x141, 0xF, 0xF, false);  // row_half_mirror
+    } else if constexpr (O == 8) {
+        return __builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false);  // row_ror:8
+    } else if constexpr (O == 16) {
+        return (uint32_t)__shfl_xor((int)x, 16);
+    } else {
+        static_assert(O == 32, "lane_xor: O in {1, 2, 4, 8, 16, 32}");
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (__lane_id() & 32) ? r[0] : r[1];
+    }
+}
+template <int O>
+__device__ __forceinline__ float lane_xor_f(float x) {
+    return __uint_as_float(lane_xor<O>(__float_as_uint(x)));
+}
+
+// One compare-exchange stage of the ascending bitonic network over the
+// wave's lanes (pairs l, l ^ STRIDE; direction from bit SIZE of l), with
+// bitonic_sort_asc's rule: the pair swaps when its lower entry is greater
+// (rising runs) or smaller (falling runs).
+template <int SIZE, int STRIDE>
+__device__ __forceinline__ float bitonic_stage(float a, int lane) {
+    const float y = lane_xor_f<STRIDE>(a);
+    const bool lower = (lane & STRIDE) == 0;
+    const float xi = lower ? a : y, xj = lower ? y : a;
+    const bool up = (lane & SIZE) == 0;
+    return (up ? (xi > xj) : (xi < xj)) ? y : a;
+}
+template <int SIZE, int STRIDE>
+__device__ __forceinline__ uint64_t bitonic_stage(uint64_t a, int lane) {
+    const uint64_t y = ((uint64_t)lane_xor<STRIDE>((uint32_t)(a >> 32)) << 32) |
+                       lane_xor<STRIDE>((uint32_t)a);
+    const bool lower = (lane & STRIDE) == 0;
+    const uint64_t xi = lower ? a : y, xj = lower ? y : a;
+    const bool up = (lane & SIZE) == 0;
+    return (up ? (xi > xj) : (xi < xj)) ? y : a;
+}
+// The network's stages of run size SIZE, strides SIZE/2 .. 1.
+template <int SIZE, int STRIDE, typename K>
+__device__ __forceinline__ K bitonic_merge(K a, int lane) {
+    a = bitonic_stage<SIZE, STRIDE>(a, lane);
+    if constexpr (STRIDE > 1) a = bitonic_merge<SIZE, STRIDE / 2>(a, lane);
+    return a;
+}
+
+// Sorts the wave's 64 distinct keys ascending, one per lane.
+__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t a, int lane) {
+    a = bitonic_merge<2, 1>(a, lane);
+    a = bitonic_merge<4, 2>(a, lane);
+    a = bitonic_merge<8, 4>(a, lane);
+    a = bitonic_merge<16, 8>(a, lane);
+    a = bitonic_merge<32, 16>(a, lane);
+    return bitonic_merge<64, 32>(a, lane);
+}
+
+// The budgets of H heads with Nk <= 64 in one wave, interleaved: lane n
+// holds block n's mass x[h] (0 for n >= Nk).  With at most 64 blocks,
+// budget_kernel's values all sit in its first wave (one entry per thread);
+// this repeats its operations on them: the wave sum of the masses (the
+// other waves' totals are zero), the shares negated and padded with +1 up to
+// P = next_pow2(Nk), the bitonic network over those P entries (the stages
+// of run sizes <= P; lanes >= P are never paired with lanes < P), the
+// inclusive scan and the first prefix reaching gamma.  Lanes outside the
+// network hold +inf.
+template <int H>
+__device__ __forceinline__ void wave_budgets(const float (&x)[H], int nk, float gamma,
+                                             int min_blocks, int lane, int (&c)[H]) {
+    const int P = next_pow2(nk);
+    float a[H];
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+        float t = lane < nk ? 0.f + x[h] : 0.f;
+        t += lane_xor_f<32>(t);
+        t += lane_xor_f<16>(t);
+        t += lane_xor_f<8>(t);
+        t += lane_xor_f<4>(t);
+        t += lane_xor_f<2>(t);
+        t += lane_xor_f<1>(t);
+        const float total = 0.f + t;
+        a[h] = lane < nk ? -(x[h] / total) : (lane < P ? 1.f : __builtin_inff());
+    }
+#define PA_BUDGET_RUN(SIZE, STRIDE)                                                 \
+    if (P >= SIZE) {                                                                \
+        _Pragma("unroll") for (int h = 0; h < H; ++h)                               \
+            a[h] = bitonic_merge<SIZE, STRIDE>(a[h], lane);                          \
+    }
+    PA_BUDGET_RUN(2, 1)
+    PA_BUDGET_RUN(4, 2)
+    PA_BUDGET_RUN(8, 4)
+    PA_BUDGET_RUN(16, 8)
+    PA_BUDGET_RUN(32, 16)
+    PA_BUDGET_RUN(64, 32)
+#undef PA_BUDGET_RUN
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+        float own = 0.f;
+        if (lane < nk) own += -a[h];
+        float incl = own;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const float y = __shfl_up(incl, o);
+            if (lane >= o) incl += y;
+        }
+        float excl = __shfl_up(incl, 1);
+        if (lane == 0) excl = 0.f;
+        float run = 0.f + excl;
+        run += -a[h];
+        const uint64_t hits = __ballot(gamma < 1.f && lane < nk && run >= gamma);
+        const int hit = hits ? __builtin_ctzll(hits) : nk;
+        int cc = (gamma < 1.f && hit < nk) ? hit + 1 : nk;
+        cc = max(cc, min_blocks);
+        c[h] = min(cc, nk);
+    }
+}
+constexpr int kFusedMaxBlocks = 64;
+constexpr int kFusedHeads = 3;   // heads per wave and round
+
 // ---------------------------------------------------------------------------
 // select: grid (Mq, G), 256 threads, dynamic LDS = P * 8 bytes (+ P * 4 for
-// ascending lists)
+// ascending lists; + 4 per head of the group when FUSED)
 // ---------------------------------------------------------------------------
 constexpr int kSelectThreads = 256;
 
+// FUSED: the counts are derived from `mass` (Nk <= 64, see wave_budget) and
+// written to head_count by block row 0; otherwise they are read from it.
+template <bool FUSED>
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
                                                                 const float* __restrict__ logA,
-                                                                const int* __restrict__ head_count,
+                                                                int* __restrict__ head_count,
+                                                                const float* __restrict__ mass,
+                                                                float gamma, int min_blocks,
                                                                 int row_ratio, int ascending,
                                                                 int* __restrict__ block_count,
                                                                 int* __restrict__ block_index) {
@@ -141,14 +286,48 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     const int P = next_pow2(ncand);
     uint64_t* key = reinterpret_cast<uint64_t*>(smem_raw);
     const float* srow = logA + ((int64_t)g * sh.mq + m) * nk;
-    // key: (order of -score) << 32 | index  -> ascending = score desc, index asc
-    for (int n = tid; n < P; n += kSelectThreads) {
-        uint64_t kk = ~0ull;
-        if (n < ncand) kk = ((uint64_t)(~float_order_key(srow[n])) << 32) | (uint32_t)n;
-        key[n] = kk;
+    int* cnt = reinterpret_cast<int*>(key + P) + (ascending ? P : 0);
+    if constexpr (FUSED) {
+        // Nk <= 64: wave 0 sorts the row's candidates in registers (one per
+        // lane; the keys are distinct, so any sorting network gives the same
+        // order) while waves 1-3 derive the group's budgets, kFusedHeads
+        // heads per wave and round
+        if (w == 0) {
+            uint64_t kk = ~0ull;
+            if (lane < ncand) kk = ((uint64_t)(~float_order_key(srow[lane])) << 32) | (uint32_t)lane;
+            kk = wave_sort_u64(kk, lane);
+            if (lane < P) key[lane] = kk;
+        } else {
+            const int i0 = g * sh.gsize, i1 = i0 + sh.gsize;
+            for (int ib = i0 + kFusedHeads * (w - 1); ib < i1; ib += 3 * kFusedHeads) {
+                float x[kFusedHeads];
+                int c[kFusedHeads];
+#pragma unroll
+                for (int h = 0; h < kFusedHeads; ++h)
+                    x[h] = (ib + h < i1 && lane < nk) ? mass[(int64_t)(ib + h) * nk + lane] : 0.f;
+                wave_budgets<kFusedHeads>(x, nk, gamma, min_blocks, lane, c);
+                if (lane == 0) {
+#pragma unroll
+                    for (int h = 0; h < kFusedHeads; ++h) {
+                        if (ib + h < i1) {
+                            cnt[ib + h - i0] = c[h];
+                            if (m == 0) head_count[ib + h] = c[h];
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    } else {
+        // key: (order of -score) << 32 | index  -> ascending = score desc, index asc
+        for (int n = tid; n < P; n += kSelectThreads) {
+            uint64_t kk = ~0ull;
+            if (n < ncand) kk = ((uint64_t)(~float_order_key(srow[n])) << 32) | (uint32_t)n;
+            key[n] = kk;
+        }
+        __syncthreads();
+        bitonic_sort_asc<uint64_t>(key, P, tid, kSelectThreads);
     }
-    __syncthreads();
-    bitonic_sort_asc<uint64_t>(key, P, tid, kSelectThreads);
     // ascending lists: rank[n] = position of block n in the rank order; each
     // thread owns E consecutive candidates
     int* rank = reinterpret_cast<int*>(key + P);
@@ -163,7 +342,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     // other); it is listed in that order, or by ascending block index
     for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
         // counts outside [0, Nk] (caller-supplied) are clamped
-        const int c = min(max(head_count[i], 0), nk);
+        const int c = min(max(FUSED ? cnt[i - g * sh.gsize] : head_count[i], 0), nk);
         // per-row ratio: ceil(c (m+1) / Nk), exact in integers (< 2^26)
         const int kk = row_ratio ? min((c * ncand + nk - 1) / nk, ncand) : min(c, ncand);
         int* out = block_index + ((int64_t)i * sh.mq + m) * nk;
@@ -249,12 +428,33 @@ hipError_t launch_select(const Shape& sh, const float* logA, const int* head_cou
     const size_t P = (size_t)next_pow2(sh.mq);
     const size_t smem = P * 8 + (ascending ? P * 4 : 0);
     if (smem > 65536) {
-        hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
+        hipError_t e = hipFuncSetAttribute((const void*)select_kernel<false>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(select_kernel, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh, logA,
-                       head_count, row_ratio, ascending, block_count, block_index);
+    // the kernel only reads head_count when not FUSED
+    hipLaunchKernelGGL(select_kernel<false>, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh,
+                       logA, const_cast<int*>(head_count), nullptr, 0.f, 0, row_ratio, ascending,
+                       block_count, block_index);
+    return hipGetLastError();
+}
+
+hipError_t launch_budget_select(const Shape& sh, const float* mass, float gamma, int min_blocks,
+                                int* head_count, const float* logA, int* block_count,
+                                int* block_index, hipStream_t st) {
+    if (sh.mq > kFusedMaxBlocks) {
+        hipError_t e = launch_budget(sh, mass, gamma, min_blocks, head_count, st);
+        if (e != hipSuccess) return e;
+        return launch_select(sh, logA, head_count, 0, 0, block_count, block_index, st);
+    }
+    const size_t smem = (size_t)next_pow2(sh.mq) * 8 + (size_t)sh.gsize * 4;
+    if (smem > 65536) {
+        hipError_t e = hipFuncSetAttribute((const void*)select_kernel<true>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(select_kernel<true>, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh,
+                       logA, head_count, mass, gamma, min_blocks, 0, 0, block_count, block_index);
     return hipGetLastError();
 }
 

@@ -530,6 +530,58 @@ def test_budget_and_topk_calls_and_budget_variants():
           flush=True)
 
 
+@pytest.mark.parametrize("n,hq,hkv,g,b", [
+    (8192, 32, 8, 4, 128),    # Nk = 64, the largest one-launch case
+    (4173, 32, 8, 4, 128),    # ragged
+    (100, 32, 8, 4, 128),     # Nk = 1
+    (129, 8, 2, 2, 128),      # Nk = 2
+    (4096, 28, 4, 7, 64),     # b = 64, Nk = 64, 4 heads per group
+    (3000, 28, 4, 1, 64),     # one group of 28 heads (7 per wave)
+    (8193, 32, 8, 4, 128),    # Nk = 65: the two launches, for the same checks
+])
+def test_one_launch_selection_matches_two(n, hq, hkv, g, b):
+    """With at most 64 key blocks proxyattn_select_budget derives the budgets
+    inside the selection launch; its counts and lists equal, bit for bit,
+    those of proxyattn_budget followed by proxyattn_select_topk (constant
+    reading, two launches), on seeded random masses and scores with exact
+    ties, zero masses, gamma from 0.3 to 1 and a minimum budget."""
+    U = _gpu()
+    from paper_2509_24745_amd import proxyattn as pa
+    prob = pa.Problem(seq_len=n, num_q_heads=hq, num_kv_heads=hkv, head_dim=128, block_size=b,
+                      num_proxy_groups=g, stride=4, dtype="bf16")
+    mq = prob.num_blocks
+    rng = np.random.default_rng(n * 31 + hq + b)
+    logA = rng.standard_normal((g, mq, mq)).astype(np.float32)
+    logA[:, :, ::3] = np.round(logA[:, :, ::3] * 2) / 2            # ties among scores
+    mass = rng.exponential(1.0, (hq, mq)).astype(np.float32)
+    mass[::3, 1::2] = 0.0                                           # zero masses
+    mass[1::4] = np.round(mass[1::4] * 4) / 4                       # ties among masses
+    mass[2] = 0.0
+    mass[2, 0] = 1.0                                                # one block holds it all
+    la, md = torch.from_numpy(logA).cuda(), torch.from_numpy(mass).cuda()
+    for gamma, min_tok in [(0.3, 0), (0.9, 0), (0.95, 3 * b), (0.999, 0), (1.0, 0)]:
+        one = pa.Buffers(prob)
+        two = pa.Buffers(prob)
+        for x in (one, two):
+            x.head_count.fill_(-7)
+            x.block_count.fill_(-7)
+            x.block_index.fill_(-7)
+        pa.proxyattn_select_budget(prob, la, md, gamma, min_tok, one.head_count, one.block_count,
+                                   one.block_index)
+        pa.proxyattn_budget(prob, md, gamma, min_tok, two.head_count)
+        pa.proxyattn_select_topk(prob, la, two.head_count, pa.TOPK_CONSTANT, two.block_count,
+                                 two.block_index)
+        torch.cuda.synchronize()
+        assert torch.equal(one.head_count, two.head_count), (gamma, min_tok)
+        assert torch.equal(one.block_count, two.block_count), (gamma, min_tok)
+        assert torch.equal(one.block_index, two.block_index), (gamma, min_tok)
+        hc = U.to_host(one.head_count)
+        assert hc.min() >= max(1, min(mq, -(-min_tok // b))) and hc.max() <= mq
+        if gamma == 1.0:
+            assert np.all(hc == mq)
+    print(f"\n[one-launch selection N={n} Nk={mq} G={g}] counts and lists identical", flush=True)
+
+
 # The diagnostic's top-k sets can differ from the oracle's only at probability
 # near-ties (both compute in fp32, in different orders); a swapped token
 # moves one score by at most one probability, which stays far below this.
