@@ -119,7 +119,7 @@ hipError_t launch_select(const Shape& sh, const float* logA, const int* head_cou
                          int row_ratio, int ascending, int* block_count, int* block_index,
                          hipStream_t st);
 // launch_budget then launch_select (rank order, constant K), as one launch
-// when Nk <= 64; the counts and lists are the same either way.
+// when Nk <= 128; the counts and lists are the same either way.
 hipError_t launch_budget_select(const Shape& sh, const float* mass, float gamma, int min_blocks,
                                 int* head_count, const float* logA, int* block_count,
                                 int* block_index, hipStream_t st);

@@ -18,10 +18,10 @@
 //   together in time are shared through the L2.  On request the same sets
 //   are listed by ascending block index instead (a rank table in LDS and a
 //   stream compaction per head).
-// budget + select in one launch (Nk <= 64, rank order): in every select
-//   workgroup, wave 0 sorts the row's candidates in registers (one per
-//   lane) while waves 1-3 derive the budgets of the group's heads, three
-//   heads at a time per wave with one block per lane, by the budget
+// budget + select in one launch (Nk <= 128, rank order): in every select
+//   workgroup, wave 0 sorts the row's candidates in registers (one or two
+//   per lane) while waves 1-3 derive the budgets of the group's heads, three
+//   heads at a time per wave with one or two blocks per lane, by the budget
 //   workgroup's own arithmetic (the same sums in the same order, the same
 //   sorting network over the same padded shares, the same prefix sums), so
 //   the counts and lists are those of the two launches for masses without
@@ -160,116 +160,140 @@ __device__ __forceinline__ float lane_xor_f(float x) {
     return __uint_as_float(lane_xor<O>(__float_as_uint(x)));
 }
 
-// One compare-exchange stage of the ascending bitonic network over the
-// wave's lanes (pairs l, l ^ STRIDE; direction from bit SIZE of l), with
-// bitonic_sort_asc's rule: the pair swaps when its lower entry is greater
-// (rising runs) or smaller (falling runs).
-template <int SIZE, int STRIDE>
-__device__ __forceinline__ float bitonic_stage(float a, int lane) {
-    const float y = lane_xor_f<STRIDE>(a);
-    const bool lower = (lane & STRIDE) == 0;
-    const float xi = lower ? a : y, xj = lower ? y : a;
-    const bool up = (lane & SIZE) == 0;
-    return (up ? (xi > xj) : (xi < xj)) ? y : a;
-}
-template <int SIZE, int STRIDE>
-__device__ __forceinline__ uint64_t bitonic_stage(uint64_t a, int lane) {
-    const uint64_t y = ((uint64_t)lane_xor<STRIDE>((uint32_t)(a >> 32)) << 32) |
-                       lane_xor<STRIDE>((uint32_t)a);
-    const bool lower = (lane & STRIDE) == 0;
-    const uint64_t xi = lower ? a : y, xj = lower ? y : a;
-    const bool up = (lane & SIZE) == 0;
-    return (up ? (xi > xj) : (xi < xj)) ? y : a;
-}
-// The network's stages of run size SIZE, strides SIZE/2 .. 1.
-template <int SIZE, int STRIDE, typename K>
-__device__ __forceinline__ K bitonic_merge(K a, int lane) {
-    a = bitonic_stage<SIZE, STRIDE>(a, lane);
-    if constexpr (STRIDE > 1) a = bitonic_merge<SIZE, STRIDE / 2>(a, lane);
-    return a;
+// The bitonic network over E * 64 entries held E per lane: entry
+// e = lane + 64 r sits in register r of the lane.  One compare-exchange
+// stage pairs e with e ^ STRIDE (between lanes for STRIDE < 64, between two
+// registers of the lane otherwise) with bitonic_sort_asc's rule: the pair
+// swaps when its lower entry is greater (rising runs, bit SIZE of e clear)
+// or smaller (falling runs).
+template <int STRIDE>
+__device__ __forceinline__ float xor_of(float a) { return lane_xor_f<STRIDE>(a); }
+template <int STRIDE>
+__device__ __forceinline__ uint64_t xor_of(uint64_t a) {
+    return ((uint64_t)lane_xor<STRIDE>((uint32_t)(a >> 32)) << 32) | lane_xor<STRIDE>((uint32_t)a);
 }
 
-// Sorts the wave's 64 distinct keys ascending, one per lane.
-__device__ __forceinline__ uint64_t wave_sort_u64(uint64_t a, int lane) {
-    a = bitonic_merge<2, 1>(a, lane);
-    a = bitonic_merge<4, 2>(a, lane);
-    a = bitonic_merge<8, 4>(a, lane);
-    a = bitonic_merge<16, 8>(a, lane);
-    a = bitonic_merge<32, 16>(a, lane);
-    return bitonic_merge<64, 32>(a, lane);
+template <int SIZE, int STRIDE, int E, typename K>
+__device__ __forceinline__ void bitonic_stage(K (&a)[E], int lane) {
+    if constexpr (STRIDE >= 64) {
+        constexpr int RS = STRIDE / 64;
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            if ((r & RS) == 0) {
+                const K xi = a[r], xj = a[r | RS];
+                const bool up = ((lane + 64 * r) & SIZE) == 0;
+                if (up ? (xi > xj) : (xi < xj)) {
+                    a[r] = xj;
+                    a[r | RS] = xi;
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const K y = xor_of<STRIDE>(a[r]);
+            const bool lower = (lane & STRIDE) == 0;
+            const K xi = lower ? a[r] : y, xj = lower ? y : a[r];
+            const bool up = ((lane + 64 * r) & SIZE) == 0;
+            a[r] = (up ? (xi > xj) : (xi < xj)) ? y : a[r];
+        }
+    }
+}
+// The stages of run size SIZE, strides SIZE/2 .. 1.
+template <int SIZE, int STRIDE, int E, typename K>
+__device__ __forceinline__ void bitonic_merge(K (&a)[E], int lane) {
+    bitonic_stage<SIZE, STRIDE>(a, lane);
+    if constexpr (STRIDE > 1) bitonic_merge<SIZE, STRIDE / 2>(a, lane);
+}
+// All run sizes 2 .. LIMIT; with `guard`, a run size only where it does not
+// exceed P (uniform), which is the network of P entries.
+template <int SIZE, int LIMIT, int E, typename K>
+__device__ __forceinline__ void bitonic_sort_regs(K (&a)[E], int lane, int P) {
+    if (SIZE <= P) bitonic_merge<SIZE, SIZE / 2>(a, lane);
+    if constexpr (SIZE < LIMIT) bitonic_sort_regs<SIZE * 2, LIMIT>(a, lane, P);
 }
 
-// The budgets of H heads with Nk <= 64 in one wave, interleaved: lane n
-// holds block n's mass x[h] (0 for n >= Nk).  With at most 64 blocks,
-// budget_kernel's values all sit in its first wave (one entry per thread);
-// this repeats its operations on them: the wave sum of the masses (the
-// other waves' totals are zero), the shares negated and padded with +1 up to
-// P = next_pow2(Nk), the bitonic network over those P entries (the stages
-// of run sizes <= P; lanes >= P are never paired with lanes < P), the
-// inclusive scan and the first prefix reaching gamma.  Lanes outside the
-// network hold +inf.
-template <int H>
-__device__ __forceinline__ void wave_budgets(const float (&x)[H], int nk, float gamma,
+// The budgets of H heads with Nk <= 64 E in one wave, interleaved: lane l
+// holds the masses x[h][r] of blocks l + 64 r (0 beyond Nk).  budget_kernel
+// keeps block n in thread n (waves 0 .. E-1 with these Nk); this repeats its
+// operations on the same values: each of its waves' sums of the masses,
+// added in wave order (the other waves' totals are zero); the shares
+// negated and padded with +1 up to P = next_pow2(Nk); the bitonic network
+// over those P entries (entries >= P, held at +inf, are never paired with
+// entries < P); each wave's inclusive scan, offset by the totals of the
+// waves before it; and the first prefix reaching gamma.
+template <int H, int E>
+__device__ __forceinline__ void wave_budgets(const float (&x)[H][E], int nk, float gamma,
                                              int min_blocks, int lane, int (&c)[H]) {
     const int P = next_pow2(nk);
-    float a[H];
+    float a[H][E];
 #pragma unroll
     for (int h = 0; h < H; ++h) {
-        float t = lane < nk ? 0.f + x[h] : 0.f;
-        t += lane_xor_f<32>(t);
-        t += lane_xor_f<16>(t);
-        t += lane_xor_f<8>(t);
-        t += lane_xor_f<4>(t);
-        t += lane_xor_f<2>(t);
-        t += lane_xor_f<1>(t);
-        const float total = 0.f + t;
-        a[h] = lane < nk ? -(x[h] / total) : (lane < P ? 1.f : __builtin_inff());
-    }
-#define PA_BUDGET_RUN(SIZE, STRIDE)                                                 \
-    if (P >= SIZE) {                                                                \
-        _Pragma("unroll") for (int h = 0; h < H; ++h)                               \
-            a[h] = bitonic_merge<SIZE, STRIDE>(a[h], lane);                          \
-    }
-    PA_BUDGET_RUN(2, 1)
-    PA_BUDGET_RUN(4, 2)
-    PA_BUDGET_RUN(8, 4)
-    PA_BUDGET_RUN(16, 8)
-    PA_BUDGET_RUN(32, 16)
-    PA_BUDGET_RUN(64, 32)
-#undef PA_BUDGET_RUN
+        float total = 0.f;
 #pragma unroll
-    for (int h = 0; h < H; ++h) {
-        float own = 0.f;
-        if (lane < nk) own += -a[h];
-        float incl = own;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const float y = __shfl_up(incl, o);
-            if (lane >= o) incl += y;
+        for (int r = 0; r < E; ++r) {
+            const int e = lane + 64 * r;
+            float t = e < nk ? 0.f + x[h][r] : 0.f;
+            t += lane_xor_f<32>(t);
+            t += lane_xor_f<16>(t);
+            t += lane_xor_f<8>(t);
+            t += lane_xor_f<4>(t);
+            t += lane_xor_f<2>(t);
+            t += lane_xor_f<1>(t);
+            total += t;
         }
-        float excl = __shfl_up(incl, 1);
-        if (lane == 0) excl = 0.f;
-        float run = 0.f + excl;
-        run += -a[h];
-        const uint64_t hits = __ballot(gamma < 1.f && lane < nk && run >= gamma);
-        const int hit = hits ? __builtin_ctzll(hits) : nk;
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const int e = lane + 64 * r;
+            a[h][r] = e < nk ? -(x[h][r] / total) : (e < P ? 1.f : __builtin_inff());
+        }
+    }
+#pragma unroll
+    for (int h = 0; h < H; ++h) bitonic_sort_regs<2, 64 * E>(a[h], lane, P);
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+        float base = 0.f;
+        int hit = nk;
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const int e = lane + 64 * r;
+            float own = 0.f;
+            if (e < nk) own += -a[h][r];
+            float incl = own;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const float y = __shfl_up(incl, o);
+                if (lane >= o) incl += y;
+            }
+            float excl = __shfl_up(incl, 1);
+            if (lane == 0) excl = 0.f;
+            float run = base + excl;
+            run += -a[h][r];
+            const uint64_t hits = __ballot(gamma < 1.f && e < nk && run >= gamma);
+            if (hit == nk && hits) hit = 64 * r + __builtin_ctzll(hits);
+            base += __shfl(incl, 63);
+        }
         int cc = (gamma < 1.f && hit < nk) ? hit + 1 : nk;
         cc = max(cc, min_blocks);
         c[h] = min(cc, nk);
     }
 }
-constexpr int kFusedMaxBlocks = 64;
-constexpr int kFusedHeads = 3;   // heads per wave and round
+// Up to 128 blocks (two entries per lane) one launch is faster than two;
+// with 256 (four per lane) the one wave's sorts take longer than the second
+// launch saves (measured: 30 against 24 us at 24K tokens).
+constexpr int kFusedMaxBlocks = 128;
+constexpr int kFusedHeads = 3;         // heads per wave and round
 
 // ---------------------------------------------------------------------------
 // select: grid (Mq, G), 256 threads, dynamic LDS = P * 8 bytes (+ P * 4 for
-// ascending lists; + 4 per head of the group when FUSED)
+// ascending lists; + 4 per head of the group when fused)
 // ---------------------------------------------------------------------------
 constexpr int kSelectThreads = 256;
 
-// FUSED: the counts are derived from `mass` (Nk <= 64, see wave_budget) and
-// written to head_count by block row 0; otherwise they are read from it.
-template <bool FUSED>
+// FE > 0 (fused, Nk <= 64 FE): the counts are derived from `mass` (see
+// wave_budgets) and written to head_count by block row 0; FE = 0: they are
+// read from head_count.
+template <int FE>
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
                                                                 const float* __restrict__ logA,
                                                                 int* __restrict__ head_count,
@@ -287,25 +311,36 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     uint64_t* key = reinterpret_cast<uint64_t*>(smem_raw);
     const float* srow = logA + ((int64_t)g * sh.mq + m) * nk;
     int* cnt = reinterpret_cast<int*>(key + P) + (ascending ? P : 0);
-    if constexpr (FUSED) {
-        // Nk <= 64: wave 0 sorts the row's candidates in registers (one per
-        // lane; the keys are distinct, so any sorting network gives the same
-        // order) while waves 1-3 derive the group's budgets, kFusedHeads
-        // heads per wave and round
+    if constexpr (FE > 0) {
+        // wave 0 sorts the row's candidates in registers (FE per lane; the
+        // keys are distinct, so any sorting network gives the same order)
+        // while waves 1-3 derive the group's budgets, kFusedHeads heads per
+        // wave and round
         if (w == 0) {
-            uint64_t kk = ~0ull;
-            if (lane < ncand) kk = ((uint64_t)(~float_order_key(srow[lane])) << 32) | (uint32_t)lane;
-            kk = wave_sort_u64(kk, lane);
-            if (lane < P) key[lane] = kk;
+            uint64_t kk[FE];
+#pragma unroll
+            for (int r = 0; r < FE; ++r) {
+                const int e = lane + 64 * r;
+                kk[r] = e < ncand ? ((uint64_t)(~float_order_key(srow[e])) << 32) | (uint32_t)e
+                                  : ~0ull;
+            }
+            bitonic_sort_regs<2, 64 * FE>(kk, lane, P);
+#pragma unroll
+            for (int r = 0; r < FE; ++r)
+                if (lane + 64 * r < P) key[lane + 64 * r] = kk[r];
         } else {
             const int i0 = g * sh.gsize, i1 = i0 + sh.gsize;
             for (int ib = i0 + kFusedHeads * (w - 1); ib < i1; ib += 3 * kFusedHeads) {
-                float x[kFusedHeads];
+                float x[kFusedHeads][FE];
                 int c[kFusedHeads];
 #pragma unroll
                 for (int h = 0; h < kFusedHeads; ++h)
-                    x[h] = (ib + h < i1 && lane < nk) ? mass[(int64_t)(ib + h) * nk + lane] : 0.f;
-                wave_budgets<kFusedHeads>(x, nk, gamma, min_blocks, lane, c);
+#pragma unroll
+                    for (int r = 0; r < FE; ++r) {
+                        const int e = lane + 64 * r;
+                        x[h][r] = (ib + h < i1 && e < nk) ? mass[(int64_t)(ib + h) * nk + e] : 0.f;
+                    }
+                wave_budgets<kFusedHeads, FE>(x, nk, gamma, min_blocks, lane, c);
                 if (lane == 0) {
 #pragma unroll
                     for (int h = 0; h < kFusedHeads; ++h) {
@@ -342,7 +377,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(Shape sh,
     // other); it is listed in that order, or by ascending block index
     for (int i = g * sh.gsize; i < (g + 1) * sh.gsize; ++i) {
         // counts outside [0, Nk] (caller-supplied) are clamped
-        const int c = min(max(FUSED ? cnt[i - g * sh.gsize] : head_count[i], 0), nk);
+        const int c = min(max(FE > 0 ? cnt[i - g * sh.gsize] : head_count[i], 0), nk);
         // per-row ratio: ceil(c (m+1) / Nk), exact in integers (< 2^26)
         const int kk = row_ratio ? min((c * ncand + nk - 1) / nk, ncand) : min(c, ncand);
         int* out = block_index + ((int64_t)i * sh.mq + m) * nk;
@@ -428,34 +463,44 @@ hipError_t launch_select(const Shape& sh, const float* logA, const int* head_cou
     const size_t P = (size_t)next_pow2(sh.mq);
     const size_t smem = P * 8 + (ascending ? P * 4 : 0);
     if (smem > 65536) {
-        hipError_t e = hipFuncSetAttribute((const void*)select_kernel<false>,
+        hipError_t e = hipFuncSetAttribute((const void*)select_kernel<0>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         if (e != hipSuccess) return e;
     }
-    // the kernel only reads head_count when not FUSED
-    hipLaunchKernelGGL(select_kernel<false>, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh,
+    // the kernel only reads head_count when not fused
+    hipLaunchKernelGGL(select_kernel<0>, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh,
                        logA, const_cast<int*>(head_count), nullptr, 0.f, 0, row_ratio, ascending,
                        block_count, block_index);
+    return hipGetLastError();
+}
+
+template <int FE>
+static hipError_t launch_fused(const Shape& sh, const float* mass, float gamma, int min_blocks,
+                               int* head_count, const float* logA, int* block_count,
+                               int* block_index, hipStream_t st) {
+    const size_t smem = (size_t)next_pow2(sh.mq) * 8 + (size_t)sh.gsize * 4;
+    if (smem > 65536) {
+        hipError_t e = hipFuncSetAttribute((const void*)select_kernel<FE>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(select_kernel<FE>, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh,
+                       logA, head_count, mass, gamma, min_blocks, 0, 0, block_count, block_index);
     return hipGetLastError();
 }
 
 hipError_t launch_budget_select(const Shape& sh, const float* mass, float gamma, int min_blocks,
                                 int* head_count, const float* logA, int* block_count,
                                 int* block_index, hipStream_t st) {
-    if (sh.mq > kFusedMaxBlocks) {
-        hipError_t e = launch_budget(sh, mass, gamma, min_blocks, head_count, st);
-        if (e != hipSuccess) return e;
-        return launch_select(sh, logA, head_count, 0, 0, block_count, block_index, st);
-    }
-    const size_t smem = (size_t)next_pow2(sh.mq) * 8 + (size_t)sh.gsize * 4;
-    if (smem > 65536) {
-        hipError_t e = hipFuncSetAttribute((const void*)select_kernel<true>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-        if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(select_kernel<true>, dim3(sh.mq, sh.g), dim3(kSelectThreads), smem, st, sh,
-                       logA, head_count, mass, gamma, min_blocks, 0, 0, block_count, block_index);
-    return hipGetLastError();
+    if (sh.mq <= 64)
+        return launch_fused<1>(sh, mass, gamma, min_blocks, head_count, logA, block_count,
+                               block_index, st);
+    if (sh.mq <= kFusedMaxBlocks)
+        return launch_fused<2>(sh, mass, gamma, min_blocks, head_count, logA, block_count,
+                               block_index, st);
+    hipError_t e = launch_budget(sh, mass, gamma, min_blocks, head_count, st);
+    if (e != hipSuccess) return e;
+    return launch_select(sh, logA, head_count, 0, 0, block_count, block_index, st);
 }
 
 }  // namespace pa

@@ -537,10 +537,14 @@ def test_budget_and_topk_calls_and_budget_variants():
     (129, 8, 2, 2, 128),      # Nk = 2
     (4096, 28, 4, 7, 64),     # b = 64, Nk = 64, 4 heads per group
     (3000, 28, 4, 1, 64),     # one group of 28 heads (7 per wave)
-    (8193, 32, 8, 4, 128),    # Nk = 65: the two launches, for the same checks
+    (8193, 32, 8, 4, 128),    # Nk = 65: two blocks per lane
+    (16384, 32, 8, 4, 128),   # Nk = 128
+    (12000, 28, 4, 2, 128),   # Nk = 94, 14 heads per group
+    (8192, 28, 4, 7, 64),     # b = 64, Nk = 128
+    (16385, 32, 8, 4, 128),   # Nk = 129: the two launches, for the same checks
 ])
 def test_one_launch_selection_matches_two(n, hq, hkv, g, b):
-    """With at most 64 key blocks proxyattn_select_budget derives the budgets
+    """With at most 128 key blocks proxyattn_select_budget derives the budgets
     inside the selection launch; its counts and lists equal, bit for bit,
     those of proxyattn_budget followed by proxyattn_select_topk (constant
     reading, two launches), on seeded random masses and scores with exact
