@@ -205,8 +205,8 @@ __device__ __forceinline__ void bitonic_merge(K (&a)[E], int lane) {
     bitonic_stage<SIZE, STRIDE>(a, lane);
     if constexpr (STRIDE > 1) bitonic_merge<SIZE, STRIDE / 2>(a, lane);
 }
-// All run sizes 2 .. LIMIT; with `guard`, a run size only where it does not
-// exceed P (uniform), which is the network of P entries.
+// The run sizes 2 .. LIMIT that do not exceed P (uniform over the wave): the
+// network of P entries.
 template <int SIZE, int LIMIT, int E, typename K>
 __device__ __forceinline__ void bitonic_sort_regs(K (&a)[E], int lane, int P) {
     if (SIZE <= P) bitonic_merge<SIZE, SIZE / 2>(a, lane);
