@@ -178,7 +178,9 @@ int proxyattn_select_budget(const proxyattn_problem* p, const float* block_logsc
 
 /*
  * Step 2 in two calls (budget variants; proxyattn_select_budget is
- * proxyattn_budget followed by proxyattn_select_topk in constant mode).
+ * proxyattn_budget followed by proxyattn_select_topk in constant mode: with
+ * up to 128 key blocks it runs both in one launch, with the same counts and
+ * lists for masses without NaN).
  *
  * proxyattn_budget: Alg. 1's per-head budget alone; arguments as for
  *     proxyattn_select_budget, head_count [Hq] int32 (out).
