@@ -992,8 +992,8 @@ def run_work_orders(wl, reps: int):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU: --gpus must be 1 (the path shards "
-                                   "by heads across GPUs only by design)"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU: --gpus must be 1 (the path "
+                                   "shards by heads across GPUs only by design)"}))
         sys.exit(2)
     if args.profile_summary:
         print(profile_summary(args.profile_summary, args.workload), end="")

@@ -55,7 +55,7 @@ extern "C" {
 /* Return codes. */
 #define PROXYATTN_OK 0
 #define PROXYATTN_E_INVALID 1     /* null pointer, negative size, gamma out of (0,1], ... */
-#define PROXYATTN_E_UNSUPPORTED 2 /* a shape or dtype this build does not implement */
+#define PROXYATTN_E_UNSUPPORTED 2 /* a shape or dtype the library does not implement */
 #define PROXYATTN_E_WORKSPACE 3   /* workspace smaller than proxyattn_workspace_size */
 #define PROXYATTN_E_HIP 4         /* a kernel launch failed (see proxyattn_last_error) */
 
