@@ -327,9 +327,10 @@ __device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F7
 // MFMAs between the LDS read of an operand fragment and the MFMA that uses it
 // (bf16 attention loop).
 constexpr int kReadLead = 2;
-// First PV segment of the bf16 loop that folds the next step's scores into
-// the running row maxima.
-constexpr int kMaxSeg0 = 4;
+// Largest sum of one lane's probabilities in a step that certainly leaves the
+// lazily rescaled reference in place: every bf16 probability is then at most
+// 2^7, so its exponent is below log2(2^7 (1 + 2^-8)) < kRescaleSlack.
+constexpr float kLazySum = 128.f;
 
 // Causal / ragged mask of one 64-key sub-tile: keys past `lim` (offset of
 // the last visible key inside the sub-tile) become -inf.  A key's offset is
@@ -493,10 +494,48 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
     if (needs_mask(nb0)) mask_tail<NT>(s_cur, qlim - nb0 * B, h);
     float mx = tile_max<NT>(s_cur) * sh.scale2;
 
+    // probabilities of the step the PV MFMAs consume next, from its scores
+    Frag pf[NT][2];
+    auto form_p = [&](const f32x16* s, float nm) {
+#pragma unroll
+        for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(s[kt][r], sh.scale2, nm)));
+    };
+    // the reference moves only when some row's max exceeds it by more than
+    // kRescaleSlack (probabilities stay < 2^8)
+    auto rescale_to = [&](float mxs) {
+        const float m_new = fmaxf(m_run, mxs);
+        const float alpha = (m_run == kNegInf) ? 0.f : fast_exp2(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        m_run = m_new;
+    };
+    // a row whose keys so far are all masked keeps m_run = -inf: its
+    // probabilities are exp2(-inf) = 0
+    auto neg_ref = [&]() { return (m_run == kNegInf) ? 0.f : -m_run; };
+    if constexpr (sizeof(T) == 2) {
+        // bf16: the first step's reference and probabilities here; later
+        // steps form theirs in the PV segments of the step before
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack)) rescale_to(mx);
+        form_p(s_cur, neg_ref());
+    }
+
     // One 64-key step.  `sc` holds the scores of step st, `sn` receives those
     // of step st+1 (two distinct register sets, used alternately, so the next
-    // scores never wait for the current softmax to free its registers).
+    // scores never wait for the current softmax to free its registers; bf16
+    // keeps `sc` only for the step's rescale check).
     auto step = [&](f32x16* sc, f32x16* sn, int st) {
+        if constexpr (sizeof(T) == 2) {
+            // a masked sub-tile (the diagonal or a ragged end, rare): its
+            // probabilities formed again from its masked scores
+            if (st > 0 && needs_mask(nb0)) {
+                mask_tail<NT>(sc, qlim - nb0 * B - (st % C::NSUB) * C::KT, h);
+                form_p(sc, neg_ref());
+            }
+        }
         // K(st+1) and V(st) have landed; every wave is done with step st-1,
         // whose slots (K(st), V(st-1)) the next copies overwrite
         wait_copies();
@@ -508,48 +547,63 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
         }
         if (st + 1 < steps) dma.issue_v(sub_src(nb1, (st + 1) % C::NSUB), slot.v((st + 1) & 1));
 
-        // lazy rescaling: the reference max moves only when some row's max
-        // exceeds it by more than kRescaleSlack (probabilities stay < 2^8)
-        if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack)) {
-            const float m_new = fmaxf(m_run, mx);
-            const float alpha = (m_run == kNegInf) ? 0.f : fast_exp2(m_run - m_new);
-            l_run *= alpha;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-            m_run = m_new;
+        if constexpr (sizeof(T) == 2) {
+            // Lazy rescaling checked after the fact.  The step's
+            // probabilities were formed against the reference of the step
+            // before (a masked sub-tile, rare, forms them again from its
+            // masked scores).  A lane whose probabilities sum to at most
+            // kLazySum holds none above it, so its row max exceeds the
+            // reference by less than kRescaleSlack and the reference stays,
+            // as the max itself would decide; otherwise (rare, and always on
+            // overflow or while a row has no reference) the row max is taken
+            // and, where the reference moves, the probabilities formed
+            // again: the same decisions and values as taking the max first.
+            float ps = prob_sum<T, NT>(pf);
+            if (__builtin_amdgcn_ballot_w64(!(ps <= kLazySum) || m_run == kNegInf)) {
+                const float mxs = tile_max<NT>(sc) * sh.scale2;
+                if (__builtin_amdgcn_ballot_w64(mxs > m_run + kRescaleSlack)) {
+                    rescale_to(mxs);
+                    form_p(sc, neg_ref());
+                    ps = prob_sum<T, NT>(pf);
+                }
+            }
+            l_run += ps;
+        } else {
+            if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleSlack)) rescale_to(mx);
         }
-        // a row whose keys so far are all masked keeps m_run = -inf: its
-        // probabilities are exp2(-inf) = 0
-        const float neg_m = (m_run == kNegInf) ? 0.f : -m_run;
+        const float neg_m = neg_ref();
 
-        // --- scores of step st+1 (MFMA) interleaved with the softmax of step
-        // st (VALU), then PV of step st (MFMA).  On the last step the scores
-        // are computed from a stale slot and discarded.
-        Frag pf[NT][2];
-        // running maxima of step st+1's raw scores (four chains); the bf16
-        // pipeline folds them in during its PV segments
-        float c4[4] = {kNegInf, kNegInf, kNegInf, kNegInf};
+        // --- scores of step st+1 (MFMA), then PV of step st (MFMA); bf16
+        // forms step st+1's probabilities (VALU) beside the PV MFMAs, fp32
+        // forms step st's beside the QK MFMAs.  On the last step the scores
+        // (and the probabilities formed from them) come from a stale slot
+        // and are discarded.
         if constexpr (sizeof(T) == 2) {
             // An explicit software pipeline over the NF = NQ + NP MFMAs of the
             // step: segment j issues MFMA j, the LDS read of the fragment that
-            // MFMA j + kReadLead consumes and a slice of the softmax, and
-            // sched_barrier keeps every segment in place, so each fragment
+            // MFMA j + kReadLead consumes and, in the PV half, a slice of the
+            // next step's probabilities; sched_barrier keeps every segment in
+            // place, so each fragment
             // arrives kReadLead MFMAs after its read was issued.  (Left to
             // itself the scheduler, short of registers, reads each fragment
             // right before its MFMA, which then waits out a whole LDS round
             // trip.)  QK MFMAs alternate between the two 32-key tiles and PV
             // MFMAs between the DT output tiles, so consecutive MFMAs never
             // feed each other; every accumulator still sums in the same order.
-            // The probability sum and the next step's row maxima are VALU work
-            // for the PV segments; an empty asm that takes each result as an
-            // operand keeps it there (the optimizer would otherwise sink it to
-            // its use after the loop, where it runs behind the last MFMA).
+            // The probabilities of step st+1 are VALU work for the PV
+            // segments: group g (pf[g / 2][g % 2], 8 keys of one 32-key tile)
+            // is formed from the scores of step st+1 in the DT segments after
+            // the last PV MFMA that reads group g of step st, the last group
+            // after the loop.  The QK segments carry no VALU work.  The row
+            // maxima the reference needs are no longer taken every step (the
+            // check at the next step's start, above); against taking them in
+            // the PV segments and forming the probabilities beside the QK
+            // MFMAs, this is -2.8 % at 128K and -2.7 % at 32K (dense -2.6 %),
+            // with bitwise the same output.  The check placed before the
+            // step's copies are issued instead was slower than the old way.
             constexpr int NQ = NT * KS, NP = NT * 2 * DT, NF = NQ + NP;
-            constexpr int EPS = NT * 16 / NQ;   // softmax elements per QK segment
-            static_assert(EPS * NQ == NT * 16, "softmax slices");
-            static_assert(NP > kMaxSeg0, "PV segments for the row maxima");
-            // score pairs folded into the maxima per PV segment
-            constexpr int MPS = (NT * 8 + NP - kMaxSeg0 - 1) / (NP - kMaxSeg0);
+            constexpr int EPP = 8 / DT;   // probabilities per PV segment
+            static_assert(EPP * DT == 8 && NP == 2 * NT * DT, "probability groups");
             const T* kb = slot.k((st + 1) & 1);
             const T* vb = slot.v(st & 1);
             auto frag = [&](int j) -> Frag {
@@ -579,33 +633,25 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
                     mma(o[p % DT], f[j], pf[p / (2 * DT)][(p / DT) % 2]);
                 }
                 if (j + kReadLead < NF) f[j + kReadLead] = frag(j + kReadLead);
-                if (j < NQ) {
+                if (j >= NQ + DT) {
+                    const int p = j - NQ, g = p / DT - 1;
+                    if (g < 2 * NT - 1) {
 #pragma unroll
-                    for (int u = 0; u < EPS; ++u) {
-                        const int x = j * EPS + u, kt = x / 16, r = x % 16;
-                        pf[kt][r >> 3][r & 7] = cvt_p<T>(fast_exp2(fmaf(sc[kt][r], sh.scale2, neg_m)));
-                    }
-                }
-                if (j == NQ) {
-                    l_run += prob_sum<T, NT>(pf);
-                    asm volatile("" : "+v"(l_run));
-                }
-                if (j >= NQ + kMaxSeg0) {
-                    // a tile's last QK MFMA was issued at least kMaxSeg0 + 1
-                    // segments earlier
-#pragma unroll
-                    for (int u = 0; u < MPS; ++u) {
-                        const int q2 = MPS * (j - NQ - kMaxSeg0) + u, kt = q2 / 8, r = 2 * (q2 % 8);
-                        if (q2 < NT * 8) {
-                            float& c = c4[(r >> 1) & 3];
-                            c = fmaxf(c, fmaxf(sn[kt][r], sn[kt][r + 1]));
-                            asm volatile("" : "+v"(c));
+                        for (int u = 0; u < EPP; ++u) {
+                            const int r = 8 * (g % 2) + EPP * (p % DT) + u;
+                            pf[g / 2][g % 2][r & 7] =
+                                cvt_p<T>(fast_exp2(fmaf(sn[g / 2][r], sh.scale2, neg_m)));
                         }
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
             __builtin_amdgcn_s_setprio(0);
+            // the last group of step st+1's probabilities (with its scores
+            // from a stale slot on the last step: formed and discarded)
+#pragma unroll
+            for (int r = 8; r < 16; ++r)
+                pf[NT - 1][1][r & 7] = cvt_p<T>(fast_exp2(fmaf(sn[NT - 1][r], sh.scale2, neg_m)));
         } else {
             qk(sn, slot.k((st + 1) & 1));
 #pragma unroll
@@ -624,14 +670,11 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
                         mma(o[dt], load_frag<T>(vt_ + (32 * dt + lc) * C::VPAD + 32 * kt + 16 * e + 8 * h),
                             pf[kt][e]);
         }
-        // --- mask and max of step st+1 (a masked sub-tile, rare, takes the
-        // maxima again after masking)
-        if (st + 1 < steps && needs_mask(nb1)) {
-            mask_tail<NT>(sn, qlim - nb1 * B - ((st + 1) % C::NSUB) * C::KT, h);
-            mx = tile_max<NT>(sn) * sh.scale2;
-        } else if constexpr (sizeof(T) == 2) {
-            mx = halves_max(fmaxf(fmaxf(c4[0], c4[1]), fmaxf(c4[2], c4[3]))) * sh.scale2;
-        } else {
+        // --- mask and max of step st+1 (fp32; bf16 masks at the start of the
+        // next step and checks its probabilities there)
+        if constexpr (sizeof(T) != 2) {
+            if (st + 1 < steps && needs_mask(nb1))
+                mask_tail<NT>(sn, qlim - nb1 * B - ((st + 1) % C::NSUB) * C::KT, h);
             mx = tile_max<NT>(sn) * sh.scale2;
         }
         nb0 = nb1;
