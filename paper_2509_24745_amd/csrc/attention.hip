@@ -325,8 +325,10 @@ struct LdsSlots {
 __device__ __forceinline__ void wait_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // MFMAs between the LDS read of an operand fragment and the MFMA that uses it
-// (bf16 attention loop).
-constexpr int kReadLead = 2;
+// (bf16 attention loop).  With the probabilities formed in the PV segments,
+// 3 is 0.3-0.7 % faster than 2 (8K to 128K, sparse and dense; 2 was the
+// better lead while the QK segments carried the softmax).
+constexpr int kReadLead = 3;
 // Largest sum of one lane's probabilities in a step that certainly leaves the
 // lazily rescaled reference in place: every bf16 probability is then at most
 // 2^7, so its exponent is below log2(2^7 (1 + 2^-8)) < kRescaleSlack.
