@@ -90,10 +90,12 @@ typedef struct proxyattn_problem {
     int64_t o_tok_stride, o_head_stride;
     /* Order in which the attention kernel takes its work items (a tuning
      * knob: results are bitwise the same under every setting).
-     * attn_order: 0 selects by problem size; 1 longest block rows first,
-     * heads fastest; 2 chunks of R block rows x all query heads; 3 chunks of
-     * R block rows x the query heads of one KV head, KV head by KV head.
-     * attn_chunk_rows: R in [1, 8192]; 0 selects by problem size.  Values
+     * attn_order: 0 selects by kernel and problem size; 1 longest block rows
+     * first, heads fastest; 2 chunks of R block rows x all query heads; 3
+     * chunks of R block rows x the query heads of one KV head, KV head by KV
+     * head, for the rows m >= Nk / 8, then the rows m < Nk / 8 of every head,
+     * longest first.  attn_chunk_rows: R in [1, 8192]; 0 selects by problem
+     * size.  Values
      * outside these ranges make every call fail with PROXYATTN_E_INVALID. */
     int32_t attn_order;
     int32_t attn_chunk_rows;

@@ -114,13 +114,17 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
     s.kv_head = p->kv_head_stride ? p->kv_head_stride : d;
     s.o_tok = p->o_tok_stride ? p->o_tok_stride : (int64_t)p->num_q_heads * d;
     s.o_head = p->o_head_stride ? p->o_head_stride : d;
-    // attention work order (tuning knob).  Default: when the re-blocked K/V
-    // takes more than 3/4 of the MALL (which the queries, lists and outputs
-    // stream through as well), KV-head-major chunks of 4 rows, so that the
-    // whole GPU works on one KV head's K/V at a time and it stays in the MALL
-    // (measured -2 % at 64K, -3 % at 128K, -10 % at 256K with 8 KV heads);
-    // otherwise row chunks of 2 rows, which balance better (KV-head-major is
-    // ~5 % slower at 8K and 1 % at 32K).
+    // attention work order (tuning knob).  Defaults: the sparse kernel takes
+    // KV-head-major chunks followed by the short rows at every size (against
+    // row chunks of 2 rows, 0.5-2 % faster from 8K to 64K with 8 KV heads;
+    // ending on the short rows keeps the workgroups' finishing times close).
+    // Chunks hold 4 rows when the re-blocked K/V takes more than 3/4 of the
+    // MALL (which the queries, lists and outputs stream through as well), so
+    // that the whole GPU works on one KV head's K/V at a time and it stays in
+    // the MALL (measured -2 % at 64K, -3 % at 128K, -10 % at 256K with 8 KV
+    // heads, against row chunks), else 2 rows.  The dense kernel, whose rows
+    // grow with m, keeps row chunks below that size (KV-head-major is 1.5 %
+    // slower at 32K and 5.6 % at 8K there) and KV-head-major above it.
     {
         // the item arithmetic multiplies R by head counts in int
         if (p->attn_order < 0 || p->attn_order > 3)
@@ -130,7 +134,8 @@ static int resolve(const proxyattn_problem* p, Shape* sh) {
                         p->attn_chunk_rows);
         const size_t kvb_bytes = (size_t)s.hkv * s.mq * 2 * s.b * s.d * esz;
         const bool big = kvb_bytes * 4 > kMallBytes * 3;
-        s.attn_order = p->attn_order ? p->attn_order - 1 : (big ? 2 : 1);
+        s.attn_order = p->attn_order ? p->attn_order - 1 : 2;
+        s.attn_order_dense = p->attn_order ? p->attn_order - 1 : (big ? 2 : 1);
         s.attn_chunk_rows = p->attn_chunk_rows ? p->attn_chunk_rows : (big ? 4 : 2);
     }
     const int64_t strides[6] = {s.q_tok, s.q_head, s.kv_tok, s.kv_head, s.o_tok, s.o_head};

@@ -177,6 +177,17 @@ struct AttnCfg {
     static constexpr int MIN_WAVES = WAVES_PER_SIMD_LDS < 1 ? 1 : (WAVES_PER_SIMD_LDS > 2 ? 2 : WAVES_PER_SIMD_LDS);
 };
 
+// Order 2 ends on the block rows m < mq / kShortRowsDiv (see attn_item).
+constexpr int kShortRowsDiv = 8;
+__host__ __device__ __forceinline__ int short_rows(const Shape& sh) { return sh.mq / kShortRowsDiv; }
+// Order 2: work-item numbers per queue in its first phase (KV-head-major
+// chunks of the rows m >= short_rows).
+__host__ __device__ __forceinline__ int kv_major_per_queue(const Shape& sh) {
+    const int R = sh.attn_chunk_rows;
+    const int chunks = sh.hkv * ((sh.mq - short_rows(sh) + R - 1) / R);
+    return ((chunks + kNumXcd - 1) / kNumXcd) * sh.rep * R;
+}
+
 // Work item number `b` (b % 8 = queue, b / 8 = position in that queue).  The
 // queues are drained by the persistent workgroups of one XCD each (workgroup
 // w serves queue w % 8: workgroups are dealt to the XCDs round-robin), so
@@ -187,10 +198,16 @@ struct AttnCfg {
 //   XCD c % 8.  Inside an XCD the query heads of one KV head on neighbouring
 //   rows are adjacent, so the K/V sub-blocks they fetch are shared through
 //   the XCD's L2; chunks dealt in turn balance the XCDs.
-// Order 2 (KV-head-major chunks): chunks of R rows x the query heads of ONE
-//   KV head, ordered KV head by KV head; chunk L runs on XCD L % 8.  At any
-//   time the whole GPU reads the K/V of about one KV head, which stays
-//   resident in the MALL.
+// Order 2 (KV-head-major chunks, then the short rows): first the rows
+//   m >= M0 = mq / 8 in chunks of R rows x the query heads of ONE KV head,
+//   ordered KV head by KV head; chunk L runs on XCD L % 8.  At any time the
+//   whole GPU reads the K/V of about one KV head, which stays resident in the
+//   MALL.  Then the rows m < M0 of every head, longest first, the query heads
+//   of one KV head together (group g on XCD g % 8).  A row sees at most m + 1
+//   blocks, so the queues end on short items and the workgroups finish close
+//   together (ending on the last KV head's rows instead left slots idle for
+//   up to a long item's time); these rows read only the first M0 key blocks
+//   of each KV head, which the MALL holds together.
 // Returns false for padding workgroups.
 __device__ __forceinline__ bool attn_item(const Shape& sh, int b, int* m_out, int* i_out) {
     const int R = sh.attn_chunk_rows;
@@ -213,16 +230,25 @@ __device__ __forceinline__ bool attn_item(const Shape& sh, int b, int* m_out, in
         *i_out = kv * sh.rep + within % sh.rep;
         return true;
     }
-    const int chunk_items = sh.rep * R;
-    const int chunks_per_kv = (sh.mq + R - 1) / R;
-    const int L = x + kNumXcd * (slot / chunk_items);
-    if (L >= sh.hkv * chunks_per_kv) return false;
-    const int kv = L / chunks_per_kv, c = L % chunks_per_kv;
-    const int within = slot % chunk_items;
-    const int m = sh.mq - 1 - (c * R + within / sh.rep);
-    if (m < 0) return false;
-    *m_out = m;
-    *i_out = kv * sh.rep + within % sh.rep;
+    const int m0 = short_rows(sh), first = kv_major_per_queue(sh);
+    if (slot < first) {
+        const int chunk_items = sh.rep * R;
+        const int chunks_per_kv = (sh.mq - m0 + R - 1) / R;
+        const int L = x + kNumXcd * (slot / chunk_items);
+        if (L >= sh.hkv * chunks_per_kv) return false;
+        const int kv = L / chunks_per_kv, c = L % chunks_per_kv;
+        const int within = slot % chunk_items;
+        const int m = sh.mq - 1 - (c * R + within / sh.rep);
+        if (m < m0) return false;
+        *m_out = m;
+        *i_out = kv * sh.rep + within % sh.rep;
+        return true;
+    }
+    const int t = slot - first;
+    const int g = x + kNumXcd * (t / sh.rep);
+    if (g >= m0 * sh.hkv) return false;
+    *m_out = m0 - 1 - g / sh.hkv;
+    *i_out = (g % sh.hkv) * sh.rep + t % sh.rep;
     return true;
 }
 
@@ -234,8 +260,8 @@ __host__ __device__ __forceinline__ int attn_items(const Shape& sh) {
         const int chunks = (sh.mq + R - 1) / R;
         return kNumXcd * ((chunks + kNumXcd - 1) / kNumXcd) * sh.hq * R;
     }
-    const int chunks = sh.hkv * ((sh.mq + R - 1) / R);
-    return kNumXcd * ((chunks + kNumXcd - 1) / kNumXcd) * sh.rep * R;
+    const int groups = short_rows(sh) * sh.hkv;
+    return kNumXcd * (kv_major_per_queue(sh) + ((groups + kNumXcd - 1) / kNumXcd) * sh.rep);
 }
 
 // Direct global -> LDS copy of one kvb sub-block (K rows, then V^T rows)
@@ -814,12 +840,14 @@ static hipError_t attn_t(const Shape& sh, bool dense, const void* q, const void*
     int g = 0;
     const int e = resident_grid(fn, 2 * B, &g);
     if (e) return (hipError_t)e;
-    const dim3 grid((unsigned)std::min(g, attn_items(sh)));
+    Shape s = sh;
+    if (dense) s.attn_order = sh.attn_order_dense;
+    const dim3 grid((unsigned)std::min(g, attn_items(s)));
     if (dense)
-        hipLaunchKernelGGL((attn_kernel<T, D, B, true>), grid, dim3(2 * B), 0, st, sh,
+        hipLaunchKernelGGL((attn_kernel<T, D, B, true>), grid, dim3(2 * B), 0, st, s,
                            (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse, queue);
     else
-        hipLaunchKernelGGL((attn_kernel<T, D, B, false>), grid, dim3(2 * B), 0, st, sh,
+        hipLaunchKernelGGL((attn_kernel<T, D, B, false>), grid, dim3(2 * B), 0, st, s,
                            (const T*)q, (const T*)kvb, bc, bi, (T*)out, lse, queue);
     return hipGetLastError();
 }

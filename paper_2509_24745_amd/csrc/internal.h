@@ -32,8 +32,10 @@ struct Shape {
     float inv_gsize;  // fl32(1 / |G|)
     int64_t q_tok, q_head, kv_tok, kv_head, o_tok, o_head;  // element strides
     // attention work order (see attn_item): 0 plain, 1 row chunks, 2
-    // KV-head-major chunks; rows per chunk
+    // KV-head-major chunks, then the short rows; the dense kernel's order;
+    // rows per chunk
     int attn_order;
+    int attn_order_dense;
     int attn_chunk_rows;
 };
 

@@ -140,7 +140,7 @@ class Problem:
     kv_head_stride: int = 0
     o_tok_stride: int = 0
     o_head_stride: int = 0
-    attn_order: int = 0        # 0 by size; 1 plain, 2 row chunks, 3 KV-head-major chunks
+    attn_order: int = 0        # 0 by kernel and size; 1 plain, 2 row chunks, 3 KV-head-major chunks then short rows
     attn_chunk_rows: int = 0   # 0 by size
 
     @property
