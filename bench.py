@@ -129,7 +129,7 @@ def cpu_baseline(wl, q, k, v, sample_rows: int):
 
 
 # sources the attention kernel is compiled from
-KERNEL_SOURCES = ("attention.hip", "common.h", "internal.h")
+KERNEL_SOURCES = ("attention.hip", "work_order.h", "common.h", "internal.h")
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "attn_traffic.json")
 
 
