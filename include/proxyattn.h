@@ -93,9 +93,9 @@ typedef struct proxyattn_problem {
      * attn_order: 0 selects by kernel and problem size; 1 longest block rows
      * first, heads fastest; 2 chunks of R block rows x all query heads; 3
      * chunks of R block rows x the query heads of one KV head, KV head by KV
-     * head, for the rows m >= Nk / 8, then the rows m < Nk / 8 of every head,
-     * longest first.  attn_chunk_rows: R in [1, 8192]; 0 selects by problem
-     * size.  Values
+     * head, for the rows m >= M0, then the rows m < M0 of every head, longest
+     * first (M0 = Nk / 8, or Nk / 4 where the re-blocked K/V is small).
+     * attn_chunk_rows: R in [1, 8192]; 0 selects by problem size.  Values
      * outside these ranges make every call fail with PROXYATTN_E_INVALID. */
     int32_t attn_order;
     int32_t attn_chunk_rows;

@@ -37,6 +37,7 @@ struct Shape {
     int attn_order;
     int attn_order_dense;
     int attn_chunk_rows;
+    int attn_short_rows;   // order 2 ends on the block rows m < attn_short_rows
 };
 
 // Number of XCDs workgroups are dealt to round-robin on MI355X.

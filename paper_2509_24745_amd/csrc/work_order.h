@@ -8,9 +8,10 @@
 
 namespace pa {
 
-// Order 2 ends on the block rows m < mq / kShortRowsDiv (see attn_item).
-constexpr int kShortRowsDiv = 8;
-__host__ __device__ __forceinline__ int short_rows(const Shape& sh) { return sh.mq / kShortRowsDiv; }
+// Order 2 ends on the block rows m < attn_short_rows (see attn_item).
+__host__ __device__ __forceinline__ int short_rows(const Shape& sh) {
+    return sh.attn_short_rows < 0 ? 0 : (sh.attn_short_rows > sh.mq ? sh.mq : sh.attn_short_rows);
+}
 // Order 2: work-item numbers per queue in its first phase (KV-head-major
 // chunks of the rows m >= short_rows).
 __host__ __device__ __forceinline__ int kv_major_per_queue(const Shape& sh) {
@@ -30,8 +31,9 @@ __host__ __device__ __forceinline__ int kv_major_per_queue(const Shape& sh) {
 //   rows are adjacent, so the K/V sub-blocks they fetch are shared through
 //   the XCD's L2; chunks dealt in turn balance the XCDs.
 // Order 2 (KV-head-major chunks, then the short rows): first the rows
-//   m >= M0 = mq / 8 in chunks of R rows x the query heads of ONE KV head,
-//   ordered KV head by KV head; chunk L runs on XCD L % 8.  At any time the
+//   m >= M0 = attn_short_rows (mq / 8 or mq / 4) in chunks of R rows x the
+//   query heads of ONE KV head, ordered KV head by KV head; chunk L runs on
+//   XCD L % 8.  At any time the
 //   whole GPU reads the K/V of about one KV head, which stays resident in the
 //   MALL.  Then the rows m < M0 of every head, longest first, the query heads
 //   of one KV head together (group g on XCD g % 8).  A row sees at most m + 1

@@ -1,6 +1,7 @@
 // Host-side enumeration of the attention kernel's work-item order (built by
 // tests/test_work_order.py with the host C++ compiler): for every order,
-// chunk size and a range of shapes, every ticket number maps to a valid
+// chunk size, count of short rows that the KV-head-major order ends on and
+// a range of shapes, every ticket number maps to a valid
 // (block row, query head) or to padding, every item is reached exactly once,
 // and the number of ticket numbers is a multiple of the queue count.
 // Prints "<cases> cases, <bad> bad" and exits non-zero on any failure.
@@ -16,7 +17,9 @@ int main() {
     for (int mq : {1, 2, 3, 7, 8, 9, 15, 16, 17, 33, 64, 100, 127, 128, 129, 255, 512, 1024, 2048})
         for (const auto& hh : heads)
             for (int order = 0; order <= 2; ++order)
-                for (int R : {1, 2, 3, 4, 7, 16, 64, 8192}) {
+                for (int R : {1, 2, 3, 4, 7, 16, 64, 8192})
+                for (int sd : {0, 1, 2, 4, 8, -1}) {
+                    if (order != 2 && sd != 8) continue;   // only order 2 reads it
                     pa::Shape sh{};
                     sh.mq = mq;
                     sh.hq = hh.first;
@@ -24,6 +27,8 @@ int main() {
                     sh.rep = sh.hq / sh.hkv;
                     sh.attn_order = order;
                     sh.attn_chunk_rows = R;
+                    // short rows: none, all, mq / 2, mq / 4, mq / 8, or out of range
+                    sh.attn_short_rows = sd == 0 ? 0 : sd == -1 ? mq + 5 : mq / sd;
                     ++cases;
                     const int n = pa::attn_items(sh);
                     if (n % pa::kNumXcd != 0) {
@@ -38,8 +43,8 @@ int main() {
                         int m = -1, i = -1;
                         if (!pa::attn_item(sh, b, &m, &i)) continue;
                         if (m < 0 || m >= mq || i < 0 || i >= sh.hq) {
-                            std::printf("mq %d hq %d hkv %d order %d R %d: ticket %d -> (%d, %d)\n",
-                                        mq, sh.hq, sh.hkv, order, R, b, m, i);
+                            std::printf("mq %d hq %d hkv %d order %d R %d short %d: ticket %d -> (%d, %d)\n",
+                                        mq, sh.hq, sh.hkv, order, R, sh.attn_short_rows, b, m, i);
                             ok = false;
                         } else {
                             ++seen[(size_t)m * sh.hq + i];
@@ -47,8 +52,9 @@ int main() {
                     }
                     for (size_t j = 0; j < seen.size() && ok; ++j)
                         if (seen[j] != 1) {
-                            std::printf("mq %d hq %d hkv %d order %d R %d: row %zu head %zu taken %d times\n",
-                                        mq, sh.hq, sh.hkv, order, R, j / sh.hq, j % sh.hq, seen[j]);
+                            std::printf("mq %d hq %d hkv %d order %d R %d short %d: row %zu head %zu taken %d times\n",
+                                        mq, sh.hq, sh.hkv, order, R, sh.attn_short_rows, j / sh.hq,
+                                        j % sh.hq, seen[j]);
                             ok = false;
                         }
                     bad += !ok;
