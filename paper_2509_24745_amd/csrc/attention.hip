@@ -631,6 +631,38 @@ __device__ __forceinline__ void attn_one(const Shape& sh, const T* __restrict__ 
 
     const float l_tot = halves_sum(l_run);
     const float inv = 1.f / l_tot;
+    if constexpr (sizeof(T) == 2 && D == 128 && B == 128) {
+        // O through LDS: the wave's 32 x D tile is written to the K slots
+        // (free once every wave is done with the last step) and read back as
+        // 16-byte row chunks, so that each store writes whole 128-byte lines
+        constexpr int OP = D + 8;
+        static_assert(2 * 32 * OP <= C::K_ELEMS, "two waves' O tiles per K slot");
+        __syncthreads();
+        T* ot = (w < 2 ? slot.k(0) : slot.k(1)) + (w & 1) * 32 * OP;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int rg = 0; rg < 4; ++rg) {
+                const int d0 = 32 * dt + 8 * rg + 4 * h;
+                const float v0 = o[dt][4 * rg + 0] * inv, v1 = o[dt][4 * rg + 1] * inv;
+                const float v2 = o[dt][4 * rg + 2] * inv, v3 = o[dt][4 * rg + 3] * inv;
+                *reinterpret_cast<uint2*>(ot + lc * OP + d0) = make_uint2(pack_bf16x2(v0, v1),
+                                                                          pack_bf16x2(v2, v3));
+            }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+            const int r = 4 * it + (lane >> 4), c = (lane & 15) * 8;
+            const u32x4 val = *reinterpret_cast<const u32x4*>(ot + r * OP + c);
+            const int tok = m * B + 32 * w + r;
+            if (tok < n_tok)
+                *reinterpret_cast<u32x4*>(out + (int64_t)tok * sh.o_tok + (int64_t)i * sh.o_head + c) = val;
+        }
+        if (qvalid && lse && h == 0) lse[(int64_t)i * n_tok + qtok] = (m_run + log2f(l_tot)) * kLn2;
+        return;
+    }
     if (qvalid) {
         T* orow = out + (int64_t)qtok * sh.o_tok + (int64_t)i * sh.o_head;
 #pragma unroll
