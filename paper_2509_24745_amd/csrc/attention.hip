@@ -178,7 +178,6 @@ struct AttnCfg {
     static constexpr int MIN_WAVES = WAVES_PER_SIMD_LDS < 1 ? 1 : (WAVES_PER_SIMD_LDS > 2 ? 2 : WAVES_PER_SIMD_LDS);
 };
 
-
 // Direct global -> LDS copy of one kvb sub-block (K rows, then V^T rows)
 // into the padded LDS layout.  One buffer_load_dwordx4 ... lds moves 64
 // consecutive 16-byte LDS slots (slot = lane); the padded layout has one
